@@ -1,0 +1,317 @@
+"""Plain CPU oracle of selective replay's hot path.  TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline
+leg import this package.  It shares no code with ``paper_2609_04875_amd`` and
+never imports it; the two meet only in the seeded generators of ``workloads``.
+
+Contents, each following the paper's definitions:
+
+* :class:`PoolModel` -- the paged KV cache's block table and free-list stack.
+  Restore of a checkpoint is a crop of the cache to the clean boundary
+  (Section 3.4 (b), Algorithm 1 restore step; "cropping is restoring", Lemma 1);
+  the replay loop of Algorithm 1 appends the sanitized suffix.  Paging itself is
+  not in the paper; the readings below fix it.
+* :func:`attention` -- fp64 prefix + causal softmax attention (C, see
+  ``pgsr_oracle.c``): the prefill form of F (Eq. (1)) over the suffix.
+* :func:`bf16_round` -- round-to-nearest-even to bfloat16, from the format's
+  definition (8 significant bits).
+* :func:`stacked_layers` -- the stacked random-init layer F used by the 70B-like
+  workload (a reading: the paper defines no layer).
+* :func:`recomputed_transitions`, :func:`replay_gain` -- Corollary 1.
+
+Readings where the paper is silent (it never describes paging):
+  R1 block-table sentinel is -1 for logical blocks >= ceil(len / B);
+  R2 the free list is a LIFO stack: push ``free[top++] = id``, pop
+     ``id = free[--top]``; the default initial stack makes pops yield 0, 1, 2, ...;
+  R3 a crop processes sequences in call order and, within one, pushes the freed
+     ids in ascending logical-block order; a crop to the current length is a
+     no-op, a crop to 0 frees every block; duplicates / out-of-range are errors
+     and change nothing (all-or-nothing);
+  R4 a reservation pops, per sequence in call order, the blocks for logical
+     indices nalloc .. ceil((len + S) / B) - 1 in increasing order.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from . import build as _build
+
+OK, EINVAL, ERANGE, ENOMEM = 0, 1, 2, 3
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        lib = ctypes.CDLL(_build.LIB)
+        f = lib.pgsr_oracle_attention
+        f.restype = ctypes.c_int
+        P = ctypes.c_void_p
+        i64, i32 = ctypes.c_int64, ctypes.c_int32
+        f.argtypes = [i64, i64, i64, i32, i32, i32, P, P, P, ctypes.c_double, P, i64, P]
+        lib.pgsr_oracle_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the C oracle uses (OMP_NUM_THREADS, else all cores)."""
+    return int(_load().pgsr_oracle_threads())
+
+
+# --------------------------------------------------------------------------- #
+# attention                                                                    #
+# --------------------------------------------------------------------------- #
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, pos0: int, scale: float,
+              rows: Optional[np.ndarray] = None) -> np.ndarray:
+    """fp64 prefix + causal attention.
+
+    q [n_q, Hq, d] holds queries at absolute positions pos0 .. pos0 + n_q - 1;
+    k, v [n_kv, Hkv, d] hold keys/values at positions 0 .. n_kv - 1 (the logical
+    cache: cropped prefix followed by the replayed tokens).  Query head h reads
+    KV head h // (Hq / Hkv).  ``rows`` (optional) lists flat indices i * Hq + h to
+    evaluate; the result is then [len(rows), d] instead of [n_q, Hq, d].
+    """
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    n_q, hq, d = q.shape
+    n_kv, hkv, d2 = k.shape
+    if d2 != d or v.shape != k.shape:
+        raise ValueError("shape mismatch")
+    if rows is None:
+        out = np.empty((n_q, hq, d), np.float64)
+        rows_p, n_rows = None, 0
+    else:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        out = np.empty((rows.shape[0], d), np.float64)
+        rows_p, n_rows = rows.ctypes.data, rows.shape[0]
+    rc = _load().pgsr_oracle_attention(n_q, pos0, n_kv, hq, hkv, d, q.ctypes.data, k.ctypes.data,
+                                       v.ctypes.data, float(scale), rows_p, n_rows, out.ctypes.data)
+    if rc != 0:
+        raise ValueError(f"oracle attention rejected its arguments (status {rc})")
+    return out
+
+
+# --------------------------------------------------------------------------- #
+# bf16 rounding from the format's definition                                   #
+# --------------------------------------------------------------------------- #
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round fp64 values to the nearest bfloat16 value, ties to even.
+
+    bfloat16 keeps 8 significant bits (1 implicit + 7 stored) and fp32's
+    exponent range: normals down to 2**-126, subnormal spacing 2**-133,
+    largest finite (2 - 2**-7) * 2**127.  Done directly from fp64 (one rounding).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros_like(x)
+    fin = np.isfinite(x) & (x != 0)
+    xf = x[fin]
+    _, e = np.frexp(np.abs(xf))               # |x| = m * 2**e, m in [0.5, 1)
+    lsb_exp = np.maximum(e - 8, -133)          # exponent of the last kept bit
+    q = np.rint(np.ldexp(xf, -lsb_exp))        # rint: round half to even
+    r = np.ldexp(q, lsb_exp)
+    big = np.abs(r) > (2.0 - 2.0 ** -7) * 2.0 ** 127
+    r[big] = np.copysign(np.inf, r[big])
+    out[fin] = r
+    out[~fin] = x[~fin]
+    return out
+
+
+# --------------------------------------------------------------------------- #
+# block table + free list                                                      #
+# --------------------------------------------------------------------------- #
+def _cdiv(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+class PoolModel:
+    """Host model of the paged KV pool's metadata (and, optionally, its data).
+
+    tables [max_seqs, max_blocks]  int32, -1 = empty (R1)
+    lens   [max_seqs]              committed tokens per sequence
+    nalloc [max_seqs]              blocks held per row (>= ceil(len/B); larger
+                                   while a reserved replay step is uncommitted)
+    free   [n_blocks]              stack storage; free[0 .. top) are free ids (R2)
+    """
+
+    def __init__(self, n_blocks: int, max_seqs: int, max_blocks: int, block_size: int,
+                 init_free_order: Optional[Sequence[int]] = None,
+                 n_layers: int = 0, n_kv_heads: int = 0, head_dim: int = 0):
+        self.B = block_size
+        self.n_blocks = n_blocks
+        self.tables = np.full((max_seqs, max_blocks), -1, np.int32)
+        self.lens = np.zeros(max_seqs, np.int32)
+        self.nalloc = np.zeros(max_seqs, np.int32)
+        if init_free_order is None:
+            self.free = np.arange(n_blocks - 1, -1, -1, dtype=np.int32)
+        else:
+            self.free = np.array(init_free_order, dtype=np.int32)
+            if sorted(self.free.tolist()) != list(range(n_blocks)):
+                raise ValueError("init_free_order must be a permutation of the block ids")
+        self.top = n_blocks
+        # optional data: [layer][block][slot][kv_head][d], fp64 (oracle's own layout)
+        self.kdata = self.vdata = None
+        if n_layers:
+            shape = (n_layers, n_blocks, block_size, n_kv_heads, head_dim)
+            self.kdata = np.full(shape, np.nan)
+            self.vdata = np.full(shape, np.nan)
+
+    # -- validation shared by the calls (all-or-nothing) --
+    def _check_seqs(self, seqs: Sequence[int]) -> int:
+        if len(set(seqs)) != len(seqs):
+            return EINVAL
+        for s in seqs:
+            if not (0 <= s < self.tables.shape[0]):
+                return EINVAL
+        return OK
+
+    def crop(self, seqs: Sequence[int], new_lens: Sequence[int]) -> int:
+        """Restore = crop (Algorithm 1 restore step): keep new_lens[i] tokens."""
+        if len(seqs) != len(new_lens):
+            return EINVAL
+        rc = self._check_seqs(seqs)
+        if rc:
+            return rc
+        for s, L in zip(seqs, new_lens):
+            if L < 0 or L > self.lens[s]:
+                return ERANGE
+        for s, L in zip(seqs, new_lens):
+            keep = _cdiv(L, self.B)
+            for j in range(keep, int(self.nalloc[s])):       # ascending logical order (R3)
+                self.free[self.top] = self.tables[s, j]
+                self.top += 1
+                self.tables[s, j] = -1
+            self.nalloc[s] = keep
+            self.lens[s] = L
+        return OK
+
+    def reserve(self, seqs: Sequence[int], q_lens: Sequence[int]) -> int:
+        """Pop the blocks that positions len .. len+S-1 need (R4)."""
+        if len(seqs) != len(q_lens):
+            return EINVAL
+        rc = self._check_seqs(seqs)
+        if rc:
+            return rc
+        need = []
+        for s, S in zip(seqs, q_lens):
+            if S < 0:
+                return EINVAL
+            blocks = _cdiv(int(self.lens[s]) + S, self.B)
+            if blocks > self.tables.shape[1]:
+                return ERANGE
+            need.append(max(0, blocks - int(self.nalloc[s])))
+        if sum(need) > self.top:
+            return ENOMEM
+        for s, n in zip(seqs, need):
+            for _ in range(n):
+                self.top -= 1
+                self.tables[s, self.nalloc[s]] = self.free[self.top]
+                self.nalloc[s] += 1
+        return OK
+
+    def commit(self, seqs: Sequence[int], q_lens: Sequence[int]) -> None:
+        for s, S in zip(seqs, q_lens):
+            self.lens[s] += S
+
+    def slot(self, seq: int, pos: int) -> Tuple[int, int]:
+        """Physical (block id, offset) of logical token ``pos`` of ``seq``."""
+        return int(self.tables[seq, pos // self.B]), pos % self.B
+
+    # -- data (oracle's own layout) --
+    def write(self, layer: int, seq: int, start: int, k: np.ndarray, v: np.ndarray) -> None:
+        for t in range(k.shape[0]):
+            b, o = self.slot(seq, start + t)
+            self.kdata[layer, b, o] = k[t]
+            self.vdata[layer, b, o] = v[t]
+
+    def gather(self, layer: int, seq: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
+        """Logical K, V of tokens 0 .. n-1 of ``seq`` read through the block table."""
+        idx = [self.slot(seq, p) for p in range(n)]
+        k = np.stack([self.kdata[layer, b, o] for b, o in idx]) if n else np.zeros((0,) + self.kdata.shape[3:])
+        v = np.stack([self.vdata[layer, b, o] for b, o in idx]) if n else np.zeros((0,) + self.vdata.shape[3:])
+        return k, v
+
+    def state(self) -> Dict[str, np.ndarray]:
+        return {"tables": self.tables.copy(), "lens": self.lens.copy(),
+                "free": self.free.copy(), "top": np.int32(self.top)}
+
+
+def prefill(pool: PoolModel, layer: int, seqs: Sequence[int], q_lens: Sequence[int],
+            q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
+            commit: bool = True) -> List[np.ndarray]:
+    """One replay call on the oracle pool: reserve, write K/V, attend, commit.
+
+    q/k/v are packed in ``seqs`` order ([sum S, H, d]).  Returns the per-sequence
+    outputs [S_i, Hq, d] (fp64).
+    """
+    rc = pool.reserve(seqs, q_lens)
+    if rc:
+        raise ValueError(f"reserve failed with status {rc}")
+    outs, off = [], 0
+    for s, S in zip(seqs, q_lens):
+        P = int(pool.lens[s])
+        pool.write(layer, s, P, k[off:off + S], v[off:off + S])
+        kk, vv = pool.gather(layer, s, P + S)
+        outs.append(attention(q[off:off + S], kk, vv, P, scale))
+        off += S
+    if commit:
+        pool.commit(seqs, q_lens)
+    return outs
+
+
+# --------------------------------------------------------------------------- #
+# Corollary 1                                                                  #
+# --------------------------------------------------------------------------- #
+def recomputed_transitions(T: int, tau: int) -> int:
+    """Transitions F runs in a replay from boundary tau - 1: T - tau + 1 (Corollary 1)."""
+    if not (1 <= tau <= T + 1):
+        raise ValueError("tau must satisfy 1 <= tau <= T + 1")
+    return T - tau + 1
+
+
+def replay_gain(T: int, tau: int) -> float:
+    """Gain over a full reset (T transitions): T / (T - tau + 1) (Corollary 1)."""
+    return T / recomputed_transitions(T, tau)
+
+
+# --------------------------------------------------------------------------- #
+# stacked random-init layers (reading: the paper defines no layer)            #
+# --------------------------------------------------------------------------- #
+def stacked_layers(x: np.ndarray, layers, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                   scale: float, pos0: int = 0, cache: Optional[List[Tuple[np.ndarray, np.ndarray]]] = None):
+    """F for the stacked workload: per layer, with bf16 storage points mirrored,
+
+        Q = bf16(x Wq), K = bf16(x Wk), V = bf16(x Wv)
+        O = bf16(attention(Q, [K_cache; K], [V_cache; V]))     (queries at pos0 ..)
+        x = bf16(x + O Wo)
+
+    ``x`` [n, d_model] are the token states at positions pos0 .. pos0+n-1 (fp64
+    holding bf16 values); ``layers`` is a list of (Wq, Wk, Wv, Wo) fp64 arrays;
+    ``cache`` gives each layer's K/V for positions 0 .. pos0-1 (the cropped
+    prefix), or None when pos0 == 0.  Returns (x_out, per-layer (K, V) of the
+    n new tokens).  Matrix products are library matmuls in fp64.
+    """
+    n = x.shape[0]
+    new_kv = []
+    for li, (wq, wk, wv, wo) in enumerate(layers):
+        q = bf16_round(x @ wq).reshape(n, n_q_heads, head_dim)
+        k = bf16_round(x @ wk).reshape(n, n_kv_heads, head_dim)
+        v = bf16_round(x @ wv).reshape(n, n_kv_heads, head_dim)
+        if pos0 > 0:
+            kc, vc = cache[li]
+            kk, vv = np.concatenate([kc[:pos0], k]), np.concatenate([vc[:pos0], v])
+        else:
+            kk, vv = k, v
+        o = bf16_round(attention(q, kk, vv, pos0, scale)).reshape(n, n_q_heads * head_dim)
+        x = bf16_round(x + o @ wo)
+        new_kv.append((k, v))
+    return x, new_kv
