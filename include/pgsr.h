@@ -1,0 +1,188 @@
+/*
+ * pgsr.h -- C ABI of the selective-replay hot path on MI355X (gfx950).
+ *
+ * The paper ("Forgetting Without Restarting: Execution-State Unlearning for
+ * Stateful LLM Agents") states forgetting as splicing a deterministic
+ * transition system R_t = F(R_{t-1}, o_t) (Section 3.1, Eq. (1)): the state up to
+ * the injection step tau is shared with the counterfactual run (Lemma 1), so a
+ * checkpoint restore is a crop of the KV cache to tau - 1 (Section 3.4 (b);
+ * Algorithm 1, restore step) and the T - tau + 1 sanitized transitions after it
+ * are replayed (Algorithm 1, replay loop; Theorem 1), which is optimal
+ * (Corollary 1).  A full reset replays all T transitions (baseline B5,
+ * Section 4.1).  Replayed content that is fixed in the counterfactual world is
+ * re-materialised by prefill (Section 3.2, after Lemma 2), which is what
+ * pgsr_replay_prefill computes.
+ *
+ * Memory model.  Every device pointer is owned by the caller (allocated, e.g.,
+ * as torch tensors), must stay valid for the pool's lifetime and is never
+ * freed or reallocated here.  The library allocates no device memory.  It keeps
+ * a HOST mirror of per-sequence length and block count and of the free-list
+ * top, updated at call time in enqueue order; one pool must not be used from
+ * two host threads at once.
+ *
+ * Device layout (elements of the pool dtype, row-major):
+ *   k_cache      [n_layers][n_blocks][n_kv_heads][block_size][head_dim]
+ *   v_cache      [n_layers][n_blocks][n_kv_heads][head_dim][block_size]
+ *                (values are stored transposed inside each block: the
+ *                 attention kernels read V along the key axis)
+ *   block_tables int32 [max_seqs][max_blocks_per_seq], -1 = no block
+ *   seq_lens     int32 [max_seqs]          committed tokens per sequence
+ *   free_list    int32 [n_blocks]          LIFO stack of free block ids
+ *   free_top     int32 [1]                 stack height
+ * Logical token p of sequence s lives in block block_tables[s][p / B] at
+ * slot p % B.  A sequence's slots at or beyond its length hold unspecified
+ * data (possibly NaN) and are never read.
+ *
+ * Errors.  Every call returns a status.  Arguments are validated against the
+ * host mirror before anything is enqueued: on PGSR_EINVAL / PGSR_ERANGE /
+ * PGSR_ENOMEM / PGSR_EUNSUPPORTED nothing was enqueued and neither the mirror
+ * nor device state changed.  PGSR_EHIP means a HIP call failed after
+ * validation; device state is then undefined and the pool must be re-created.
+ * pgsr_last_error() describes the most recent failure on the calling thread.
+ *
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Every call
+ * only enqueues work and returns without synchronising, except
+ * pgsr_pool_create and pgsr_pool_refresh, which block.
+ */
+#ifndef PGSR_H
+#define PGSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    PGSR_OK = 0,
+    PGSR_EINVAL = 1,        /* bad argument: null pointer, bad id, duplicate sequence */
+    PGSR_ERANGE = 2,        /* a length outside what the sequence or its table row allows */
+    PGSR_ENOMEM = 3,        /* the free list holds too few blocks */
+    PGSR_EUNSUPPORTED = 4,  /* a geometry or dtype with no kernel */
+    PGSR_EHIP = 5           /* a HIP runtime call or launch failed */
+};
+
+enum { PGSR_F32 = 0, PGSR_BF16 = 1 };
+
+/* flags */
+#define PGSR_COMMIT 1u        /* replay: advance each sequence's length by its q_len */
+#define PGSR_POISON 2u        /* crop: fill released slots with NaN (debug aid) */
+
+typedef struct pgsr_pool pgsr_pool;
+
+/* Text of the last failure on this thread; "" if none.  Valid until the next
+ * call on this thread. */
+const char *pgsr_last_error(void);
+
+/* Library ABI version (increments on incompatible changes). */
+int pgsr_abi_version(void);
+
+/*
+ * Create a pool over caller-owned device memory and initialise its device
+ * state: every table entry -1, every length 0, free_list = the initial stack,
+ * free_top = n_blocks.  init_free_order (HOST, nullable, n_blocks entries) is
+ * the stack from bottom to top and must be a permutation of 0 .. n_blocks-1;
+ * NULL means n_blocks-1 .. 0, so pops yield 0, 1, 2, ....  The KV caches are
+ * not touched.  workspace (device, nullable) is scratch for split-key partial
+ * results, workspace_bytes long (see pgsr_workspace_bytes); NULL disables
+ * key splitting.  Supported: dtype PGSR_F32 or PGSR_BF16, head_dim 64 or 128,
+ * block_size 16, 32 or 64, n_q_heads a multiple of n_kv_heads.  Blocks.
+ */
+int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                     int32_t block_size, int32_t dtype, int32_t n_blocks, int32_t max_seqs,
+                     int32_t max_blocks_per_seq, void *k_cache, void *v_cache,
+                     int32_t *block_tables, int32_t *seq_lens, int32_t *free_list,
+                     int32_t *free_top, void *workspace, size_t workspace_bytes,
+                     const int32_t *init_free_order, void *stream, pgsr_pool **out);
+
+/* Release the host object; device memory is the caller's. NULL is a no-op. */
+int pgsr_pool_destroy(pgsr_pool *pool);
+
+/* Re-read the host mirror from device state (blocking).  For callers that
+ * restore block_tables / seq_lens / free_list / free_top themselves, e.g. by
+ * copying a saved pre-crop state back; a row's block count is taken as the
+ * number of leading non-negative entries. */
+int pgsr_pool_refresh(pgsr_pool *pool, void *stream);
+
+/* Host-mirror queries (no device access). */
+int pgsr_seq_len(const pgsr_pool *pool, int32_t seq, int32_t *len_out);
+int pgsr_free_blocks(const pgsr_pool *pool, int32_t *n_out);
+
+/* Bytes of workspace that let a replay of up to max_total_q query tokens use
+ * up to max_splits key splits. */
+size_t pgsr_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int64_t max_total_q,
+                            int32_t max_splits);
+
+/*
+ * Restore = crop (Algorithm 1, restore step; Section 3.4 (b); Lemma 1): for
+ * each i, keep the first new_lens[i] tokens of sequence seqs[i]
+ * (0 <= new_lens[i] <= its length).  Table entries from ceil(new_len / B) on
+ * become -1 and those block ids are pushed onto the free list, sequences in
+ * call order, ascending logical block within a sequence; a crop to the current
+ * length is a no-op and a crop to 0 releases every block.  KV data of the kept
+ * tokens is not touched.  seqs and new_lens are HOST arrays of n entries; a
+ * duplicate sequence is PGSR_EINVAL.  flags: 0 or PGSR_POISON.
+ * All-or-nothing.
+ */
+int pgsr_kv_crop(pgsr_pool *pool, int32_t n, const int32_t *seqs, const int32_t *new_lens,
+                 unsigned flags, void *stream);
+
+/*
+ * One layer of F over the sanitized suffix, prefill form (Algorithm 1, replay
+ * loop; Theorem 1; re-materialisation by prefill, Section 3.2 after Lemma 2).
+ * For each i, with P_i the committed length of seqs[i] and S_i = q_lens[i]:
+ *   1. blocks for positions P_i .. P_i+S_i-1 are popped from the free list when
+ *      the row holds fewer (so the first layer of a step reserves them);
+ *   2. the S_i new keys/values are written to positions P_i .. P_i+S_i-1 of
+ *      `layer` (filling the partial tail block first);
+ *   3. o receives, for the query at absolute position p = P_i + t and query
+ *      head h (KV head h / (n_q_heads / n_kv_heads)), softmax attention over
+ *      keys 0 .. p:  o = sum_j softmax_j(softmax_scale * q.k_j) v_j.
+ * q, o : [sum S_i][n_q_heads][head_dim];  k, v : [sum S_i][n_kv_heads][head_dim],
+ * device, pool dtype, packed in seqs order.  seqs, q_lens: HOST arrays.
+ * flags & PGSR_COMMIT adds S_i to each length (set it on the last layer of a
+ * step) and sum S_i to *recomputed_tokens (HOST, nullable) -- the count of
+ * Corollary 1.  Outputs are bitwise reproducible run to run and depend only on
+ * each query's absolute position, not on how the suffix is batched.
+ */
+int pgsr_replay_prefill(pgsr_pool *pool, int32_t layer, int32_t n, const int32_t *seqs,
+                        const int32_t *q_lens, const void *q, const void *k, const void *v,
+                        void *o, float softmax_scale, unsigned flags,
+                        int64_t *recomputed_tokens, void *stream);
+
+/*
+ * Full reset (baseline B5, Section 4.1; T invocations of F, Corollary 1): on
+ * layer 0 the sequences are first cropped to 0, then the whole sanitized
+ * trajectory (lens[i] tokens) is replayed exactly as pgsr_replay_prefill does
+ * with P_i = 0.  Same arguments and validation; all-or-nothing.
+ */
+int pgsr_full_reset_prefill(pgsr_pool *pool, int32_t layer, int32_t n, const int32_t *seqs,
+                            const int32_t *lens, const void *q, const void *k, const void *v,
+                            void *o, float softmax_scale, unsigned flags,
+                            int64_t *recomputed_tokens, void *stream);
+
+/*
+ * Kernel timing for profiling tools.  With timing on, every replay / full-reset
+ * call records HIP events on its stream around its append launches and around
+ * its attention launches (a few microseconds of overhead per call).
+ * pgsr_pool_last_times waits for the most recent such call's events and
+ * returns the GPU time of its append and attention kernels in milliseconds.
+ */
+int pgsr_pool_enable_timing(pgsr_pool *pool, int on);
+int pgsr_pool_last_times(pgsr_pool *pool, float *append_ms, float *attention_ms);
+
+/*
+ * Dense projection of the stacked-layer transition F (theta in Eq. (1)):
+ * Y[m][n] = X[m][k] . W[k][n] (+ R[m][n] when R != NULL), bf16 row-major
+ * device arrays, fp32 accumulation, one round-to-nearest-even store.  R may
+ * alias Y.  m, n, k >= 0; n and k must be multiples of 8.
+ */
+int pgsr_gemm_bf16(int32_t m, int32_t n, int32_t k, const void *x, const void *w,
+                   const void *r, void *y, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PGSR_H */

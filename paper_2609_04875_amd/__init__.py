@@ -1,0 +1,15 @@
+"""MI355X-native hot path of Provenance-Guided Selective Replay.
+
+Restore a checkpoint by cropping a paged KV cache to the injection boundary
+tau - 1 (Algorithm 1, restore step; Lemma 1), then replay the T - tau + 1
+sanitized transitions as a prefix + causal prefill against the kept prefix
+(Algorithm 1, replay loop; Theorem 1; Corollary 1).  The work runs in the HIP
+kernels of ``lib/libpgsr.so`` behind the C ABI of ``include/pgsr.h``; this
+package only allocates device memory with torch and marshals arguments.
+"""
+from ._native import (BF16, COMMIT, EHIP, EINVAL, ENOMEM, EUNSUPPORTED, ERANGE, F32, OK, POISON,
+                      PgsrError)
+from .pool import KVPool, gemm_bf16
+
+__all__ = ["KVPool", "gemm_bf16", "PgsrError", "OK", "EINVAL", "ERANGE", "ENOMEM",
+           "EUNSUPPORTED", "EHIP", "F32", "BF16", "COMMIT", "POISON"]

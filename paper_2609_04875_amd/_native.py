@@ -1,0 +1,82 @@
+"""ctypes binding of libpgsr.so (the C ABI in include/pgsr.h).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  Importing this module fails loudly when the library is not built;
+there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "lib", "libpgsr.so")
+
+OK, EINVAL, ERANGE, ENOMEM, EUNSUPPORTED, EHIP = range(6)
+F32, BF16 = 0, 1
+COMMIT, POISON = 1, 2
+
+EXPORTS = (
+    "pgsr_last_error", "pgsr_abi_version", "pgsr_pool_create", "pgsr_pool_destroy",
+    "pgsr_pool_refresh", "pgsr_seq_len", "pgsr_free_blocks", "pgsr_workspace_bytes",
+    "pgsr_kv_crop", "pgsr_replay_prefill", "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
+    "pgsr_pool_enable_timing", "pgsr_pool_last_times",
+)
+
+
+class PgsrError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"pgsr status {code}: {msg}")
+        self.code = code
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python paper_2609_04875_amd/build.py` "
+            "(or __graft_entry__.build()); there is no fallback path")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, u32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_float
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    lib.pgsr_last_error.restype = ctypes.c_char_p
+    lib.pgsr_last_error.argtypes = []
+    lib.pgsr_abi_version.restype = ctypes.c_int
+    lib.pgsr_pool_create.restype = ctypes.c_int
+    lib.pgsr_pool_create.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P, P,
+                                     ctypes.c_size_t, i32p, P, ctypes.POINTER(P)]
+    lib.pgsr_pool_destroy.restype = ctypes.c_int
+    lib.pgsr_pool_destroy.argtypes = [P]
+    lib.pgsr_pool_refresh.restype = ctypes.c_int
+    lib.pgsr_pool_refresh.argtypes = [P, P]
+    lib.pgsr_seq_len.restype = ctypes.c_int
+    lib.pgsr_seq_len.argtypes = [P, i32, i32p]
+    lib.pgsr_free_blocks.restype = ctypes.c_int
+    lib.pgsr_free_blocks.argtypes = [P, i32p]
+    lib.pgsr_workspace_bytes.restype = ctypes.c_size_t
+    lib.pgsr_workspace_bytes.argtypes = [i32, i32, i64, i32]
+    lib.pgsr_kv_crop.restype = ctypes.c_int
+    lib.pgsr_kv_crop.argtypes = [P, i32, i32p, i32p, u32, P]
+    for name in ("pgsr_replay_prefill", "pgsr_full_reset_prefill"):
+        f = getattr(lib, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [P, i32, i32, i32p, i32p, P, P, P, P, f32, u32, ctypes.POINTER(i64), P]
+    lib.pgsr_pool_enable_timing.restype = ctypes.c_int
+    lib.pgsr_pool_enable_timing.argtypes = [P, ctypes.c_int]
+    lib.pgsr_pool_last_times.restype = ctypes.c_int
+    lib.pgsr_pool_last_times.argtypes = [P, ctypes.POINTER(f32), ctypes.POINTER(f32)]
+    lib.pgsr_gemm_bf16.restype = ctypes.c_int
+    lib.pgsr_gemm_bf16.argtypes = [i32, i32, i32, P, P, P, P, P]
+    return lib
+
+
+lib = _load()
+
+
+def check(code: int) -> None:
+    if code != OK:
+        raise PgsrError(code, lib.pgsr_last_error().decode())
+
+
+def int32_array(values):
+    values = [int(v) for v in values]
+    return (ctypes.c_int32 * max(1, len(values)))(*values)

@@ -1,0 +1,284 @@
+// bf16 prefix + causal prefill attention on CDNA4 matrix cores (gfx950).
+//
+// Work decomposition.  A workgroup of NW wave64s owns one KV head g and a tile
+// of TW = NW*32/G consecutive suffix tokens together with the G query heads
+// that share g (GQA packing: every query row of the workgroup reads the same
+// K/V tiles).  Each wave owns 32 query rows (token, head).  blockIdx.x =
+// tile * n_kv_heads + g, so with 8 KV heads all tiles of one head land on the
+// same XCD (workgroups are dealt to the 8 XCDs round-robin) and share that
+// XCD's L2 copy of the head's keys and values.  Tiles are issued costliest
+// first (sequences sorted by work on the host, tiles within a sequence from
+// the last, longest-context one down).
+//
+// Per key tile (KT = 64 keys at absolute positions kb .. kb+63):
+//   * K and V^T are gathered through the block table from HBM into registers
+//     one tile ahead, then stored to a double-buffered LDS tile (one barrier
+//     per tile).  Keys at or beyond the sequence length are zero-filled, never
+//     loaded.
+//   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = Q^T
+//     held in registers for the whole kernel).  In the 32x32 accumulator a lane
+//     holds one query column and 16 keys, so the row max and row sum are
+//     in-lane reductions plus one exchange between the two 32-lane halves.
+//   * Online softmax in the base-2 domain (log2(e) folded into the scale);
+//     the causal mask is a select to -inf on diagonal tiles only.  The O
+//     rescale is skipped when no row's maximum moved (alpha == 1 exactly, so
+//     the result is bitwise the same as always rescaling).
+//   * O^T += V^T P^T with the same MFMA (A = V^T rows from LDS, B = P^T taken
+//     straight from the S^T registers after rounding to bf16).  The reduction
+//     index of a B operand must match the A operand's, and a lane's S^T
+//     registers hold keys {4h..4h+3, 8+4h..8+4h+3} of each 16-key group (h =
+//     lane half); V^T is therefore stored in LDS with the 4-key chunks of every
+//     16-key group in the order [0, 2, 1, 3], which makes those 8 keys one
+//     contiguous 16-byte LDS read.
+// Key tiles sit at absolute positions and rows never interact, so a query's
+// output bits depend only on its absolute position: selective replay and full
+// reset agree bitwise, and repeated runs are bitwise identical.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "internal.h"
+
+namespace pgsr {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kNW = 4;   // waves per workgroup
+constexpr int kKT = 64;  // keys per tile
+
+__device__ inline float xor32(float x) { return __shfl_xor(x, 32, 64); }
+
+// Zero 16-bit elements e (0..7) of a 16-byte chunk for which pos0 + e >= limit.
+__device__ inline u32x4 zero_tail(u32x4 v, int pos0, int limit) {
+  const int keep = limit - pos0;  // elements to keep, < 8 here
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const int e0 = 2 * w;
+    uint32_t m = 0;
+    if (e0 < keep) m |= 0x0000FFFFu;
+    if (e0 + 1 < keep) m |= 0xFFFF0000u;
+    v[w] &= m;
+  }
+  return v;
+}
+
+template <int D, int NW>
+__global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
+  constexpr int KT = kKT;
+  constexpr int KLD = D + 8;    // LDS row stride of the K tile (elements)
+  constexpr int VLD = KT + 8;   // LDS row stride of the V^T tile (elements)
+  constexpr int NT = NW * 64;
+  constexpr int KCH = KT * D / 8 / NT;  // 16-byte K chunks per thread per tile
+  constexpr int VCH = D * KT / 8 / NT;  // 16-byte V chunks per thread per tile
+  static_assert(KCH * NT * 8 == KT * D && VCH * NT * 8 == KT * D, "tile split");
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][KT * KLD];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][D * VLD];
+
+  const int hkv = a.n_kv_heads;
+  const int g = blockIdx.x % hkv;
+  const int tile = blockIdx.x / hkv;
+  int ei = 0;
+  while (ei + 1 < a.n && a.e[ei + 1].tile_start <= tile) ++ei;
+  const AttnEntry e = a.e[ei];
+  const int G = a.n_q_heads / hkv;
+  const int TW = NW * 32 / G;                       // tokens per tile
+  const int n_tiles_e = (e.q_len + TW - 1) / TW;
+  const int lt = n_tiles_e - 1 - (tile - e.tile_start);
+  const int t0 = lt * TW;
+
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, lane = tid & 63, r = lane & 31, hh = lane >> 5;
+  const int tok = t0 + w * (32 / G) + r / G;
+  const int hq = g * G + r % G;
+  const bool valid = tok < e.q_len;
+  const int qpos = valid ? e.prefix + tok : -1;
+  const int t_last = min(e.q_len, t0 + TW) - 1;
+  const int kv_len = e.prefix + e.q_len;
+  const int key_end = e.prefix + t_last + 1;
+  const int n_kt = (key_end + KT - 1) / KT;
+  const int first_q = e.prefix + t0;               // smallest query position here
+
+  // Q^T operand: lane holds Q[row][16*ds + 8*hh .. +7] for each ds.
+  bf16x8 qb[D / 16];
+  {
+    const uint16_t* qg =
+        (const uint16_t*)a.q + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 8 * hh;
+#pragma unroll
+    for (int ds = 0; ds < D / 16; ++ds) {
+      u32x4 raw = valid ? *(const u32x4*)(qg + 16 * ds) : u32x4{0, 0, 0, 0};
+      qb[ds] = __builtin_bit_cast(bf16x8, raw);
+    }
+  }
+
+  const int B = a.block_size;
+  const int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
+  const int64_t head_base = (int64_t)a.layer * a.n_blocks * hkv + g;  // + id * hkv
+  const uint16_t* kc = (const uint16_t*)a.k_cache;
+  const uint16_t* vc = (const uint16_t*)a.v_cache;
+  const int cpb = B / 8;  // 16-byte chunks per V^T row of one block
+
+  u32x4 kreg[KCH], vreg[VCH];
+  auto load_tile = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * NT;
+      const int key = c / (D / 8), col = c % (D / 8);
+      const int pos = kb + key;
+      u32x4 val = {0, 0, 0, 0};
+      if (pos < kv_len) {
+        const int32_t id = row[pos / B];
+        val = *(const u32x4*)(kc + ((head_base + (int64_t)id * hkv) * B + pos % B) * D + col * 8);
+      }
+      kreg[i] = val;
+    }
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = tid + i * NT;
+      const int bi = c / (D * cpb), rem = c % (D * cpb);
+      const int dd = rem / cpb, ck = rem % cpb;
+      const int pos0 = kb + bi * B + ck * 8;
+      u32x4 val = {0, 0, 0, 0};
+      if (pos0 < kv_len) {
+        const int32_t id = row[pos0 / B];
+        val = *(const u32x4*)(vc + ((head_base + (int64_t)id * hkv) * D + dd) * B + pos0 % B);
+        if (pos0 + 8 > kv_len) val = zero_tail(val, pos0, kv_len);
+      }
+      vreg[i] = val;
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * NT;
+      const int key = c / (D / 8), col = c % (D / 8);
+      *(u32x4*)&k_lds[buf][key * KLD + col * 8] = kreg[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = tid + i * NT;
+      const int bi = c / (D * cpb), rem = c % (D * cpb);
+      const int dd = rem / cpb, ck = rem % cpb;
+      const int key0 = bi * B + ck * 8;            // tile-relative, multiple of 8
+      const int base = dd * VLD + (key0 & ~15);
+      const int half = (key0 >> 3) & 1;            // 4-key chunks 2h, 2h+1 -> slots h, h+2
+      *(u32x2*)&v_lds[buf][base + 4 * half] = u32x2{vreg[i][0], vreg[i][1]};
+      *(u32x2*)&v_lds[buf][base + 4 * half + 8] = u32x2{vreg[i][2], vreg[i][3]};
+    }
+  };
+
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
+  float m = -INFINITY, l = 0.f;
+  const float c2 = a.scale_log2;
+
+  load_tile(0);
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int buf = kt & 1;
+    const int kb = kt * KT;
+    store_tile(buf);
+    __syncthreads();
+    if (kt + 1 < n_kt) load_tile(kb + KT);
+
+    // S^T = K Q^T for keys kb .. kb+63 (two 32-key halves).
+    f32x16 s[2];
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh) {
+      s[kh] = f32x16{};
+      const uint16_t* kp = &k_lds[buf][(kh * 32 + r) * KLD + 8 * hh];
+#pragma unroll
+      for (int ds = 0; ds < D / 16; ++ds) {
+        bf16x8 ka = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 16 * ds));
+        s[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[ds], s[kh], 0, 0, 0);
+      }
+    }
+    // Causal mask (select) where some key may lie past some row's position.
+    if (kb + KT - 1 > first_q) {
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kb + kh * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+          s[kh][i] = key > qpos ? -INFINITY : s[kh][i];
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kh][i]);
+    mx = fmaxf(mx, xor32(mx));
+    const float m_new = fmaxf(m, mx * c2);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m - m_use);
+    float psum = 0.f;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[kh][i], c2, -m_use));
+        s[kh][i] = p;
+        psum += p;
+      }
+    l = fmaf(l, alpha, psum);
+    m = m_new;
+    if (__ballot(alpha != 1.f)) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
+    }
+    // O^T += V^T P^T, 16 keys per step.
+#pragma unroll
+    for (int ks = 0; ks < KT / 16; ++ks) {
+      const int kh = ks >> 1, o8 = (ks & 1) * 8;
+      f32x8 pv = {s[kh][o8 + 0], s[kh][o8 + 1], s[kh][o8 + 2], s[kh][o8 + 3],
+                  s[kh][o8 + 4], s[kh][o8 + 5], s[kh][o8 + 6], s[kh][o8 + 7]};
+      const bf16x8 pb = __builtin_convertvector(pv, bf16x8);
+      const uint16_t* vp = &v_lds[buf][r * VLD + ks * 16 + 8 * hh];
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        bf16x8 va = __builtin_bit_cast(bf16x8, *(const u32x4*)(vp + db * 32 * VLD));
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, oacc[db], 0, 0, 0);
+      }
+    }
+  }
+
+  const float l_tot = l + xor32(l);
+  if (valid) {
+    const float inv = 1.f / l_tot;
+    uint16_t* op = (uint16_t*)a.o + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        f32x4 v4 = {oacc[db][4 * i4 + 0] * inv, oacc[db][4 * i4 + 1] * inv,
+                    oacc[db][4 * i4 + 2] * inv, oacc[db][4 * i4 + 3] * inv};
+        *(bf16x4*)(op + db * 32 + 8 * i4) = __builtin_convertvector(v4, bf16x4);
+      }
+  }
+}
+
+}  // namespace
+
+int attn_bf16_tile_tokens(int, int group) { return kNW * 32 / group; }
+
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
+  dim3 grid(a.n_tiles * a.n_kv_heads);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL((attn_bf16_kernel<128, kNW>), grid, dim3(kNW * 64), 0, s, a);
+  else if (a.head_dim == 64)
+    hipLaunchKernelGGL((attn_bf16_kernel<64, kNW>), grid, dim3(kNW * 64), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace pgsr

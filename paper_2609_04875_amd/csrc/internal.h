@@ -1,0 +1,117 @@
+// Internal interface between the host runtime (pgsr_host.cpp) and the kernels.
+// Per-call sequence descriptors travel in the kernel-argument segment, so a
+// call carries no host->device copy; calls with more sequences are split into
+// several launches of at most kMaxSeqsPerLaunch sequences each.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace pgsr {
+
+constexpr int kMaxSeqsPerLaunch = 64;
+
+// ---------------------------------------------------------------- crop ---- //
+struct CropEntry {
+  int32_t seq;       // row of the block table
+  int32_t new_len;   // tokens kept
+  int32_t keep;      // ceil(new_len / B): table entries kept
+  int32_t nalloc;    // entries held before the crop
+  int32_t push_off;  // where this sequence's freed ids start above top_before
+};
+
+struct CropArgs {
+  int32_t* tables;
+  int32_t* lens;
+  int32_t* free_list;
+  int32_t* free_top;
+  int32_t max_bps;
+  int32_t top_before;  // stack height when this launch starts
+  int32_t top_after;   // stack height when this launch ends
+  int32_t n;
+  CropEntry e[kMaxSeqsPerLaunch];
+};
+
+// Debug aid: NaN-fill every slot a crop released (freed blocks in all layers,
+// and the tail slots of a kept partial block).
+struct PoisonArgs {
+  void* k_cache;
+  void* v_cache;
+  const int32_t* tables;
+  const int32_t* free_list;
+  int32_t max_bps, n_layers, n_blocks, n_kv_heads, block_size, head_dim, elem_bytes;
+  int32_t top_before;
+  int32_t n;
+  CropEntry e[kMaxSeqsPerLaunch];
+};
+
+// --------------------------------------------------------- reserve+append - //
+struct AppendEntry {
+  int32_t seq;
+  int32_t prefix;         // committed length P (first new position)
+  int32_t q_len;          // S new tokens
+  int32_t q_off;          // first row of this sequence in the packed k/v inputs
+  int32_t nalloc_before;  // table entries held before this call's reservation
+  int32_t stack_before;   // stack height before this sequence's pops
+  int32_t lb_first;       // first logical block touched: P / B
+  int32_t item_start;     // prefix sum of logical blocks touched over entries
+};
+
+struct AppendArgs {
+  void* k_cache;
+  void* v_cache;
+  const void* k_in;
+  const void* v_in;
+  int32_t* tables;
+  int32_t* lens;
+  const int32_t* free_list;
+  int32_t* free_top;
+  int32_t max_bps, n_blocks, n_kv_heads, block_size, head_dim, layer;
+  int32_t commit;
+  int32_t write_top;   // 1: this launch writes free_top = top_after
+  int32_t top_after;
+  int32_t n;
+  int32_t n_items;
+  AppendEntry e[kMaxSeqsPerLaunch];
+};
+
+// -------------------------------------------------------------- attention - //
+struct AttnEntry {
+  int32_t seq;
+  int32_t prefix;      // P: queries sit at absolute positions P .. P+S-1
+  int32_t q_len;       // S
+  int32_t q_off;       // first row of this sequence in q / o
+  int32_t tile_start;  // prefix sum of query tiles over entries
+};
+
+struct AttnArgs {
+  const void* q;
+  void* o;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* tables;
+  int32_t max_bps, n_blocks, n_q_heads, n_kv_heads, block_size, head_dim, layer;
+  float scale_log2;    // softmax_scale * log2(e)
+  int32_t n;
+  int32_t n_tiles;
+  AttnEntry e[kMaxSeqsPerLaunch];
+};
+
+// Query tokens per workgroup tile for each kernel (the host sizes grids with these).
+int attn_f32_tile_tokens(int head_dim, int group);
+int attn_bf16_tile_tokens(int head_dim, int group);
+
+hipError_t launch_crop(const CropArgs& a, hipStream_t s);
+hipError_t launch_poison(const PoisonArgs& a, hipStream_t s);
+hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s);
+hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
+hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
+                            int32_t* free_list, int32_t n_blocks, int32_t* free_top,
+                            hipStream_t s);
+hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
+                            void* y, hipStream_t s);
+
+}  // namespace pgsr

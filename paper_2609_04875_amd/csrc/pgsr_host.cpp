@@ -1,0 +1,546 @@
+// Host runtime of the C ABI declared in include/pgsr.h: argument validation
+// against a host mirror of the pool, block reservation bookkeeping, and kernel
+// launches on the caller's stream.  Every check runs before the first launch,
+// so a rejected call changes neither the mirror nor device memory.
+#include "pgsr.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace pgsr;
+
+struct pgsr_pool {
+  int32_t n_layers, hq, hkv, d, B, dtype, n_blocks, max_seqs, max_bps;
+  void* k_cache;
+  void* v_cache;
+  int32_t* tables;
+  int32_t* lens;
+  int32_t* free_list;
+  int32_t* free_top;
+  void* workspace;
+  size_t workspace_bytes;
+  // host mirror
+  std::vector<int32_t> h_len, h_nalloc;
+  int32_t h_top;
+  // optional kernel timing: events around the append and attention launches
+  bool timing = false, timed_call = false;
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return PGSR_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(PGSR_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline int32_t cdiv(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
+
+int elem_bytes(const pgsr_pool* p) { return p->dtype == PGSR_F32 ? 4 : 2; }
+
+// Distinct, in-range sequence ids.
+int check_seqs(const pgsr_pool* p, int32_t n, const int32_t* seqs) {
+  std::vector<char> seen(p->max_seqs, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = seqs[i];
+    if (s < 0 || s >= p->max_seqs)
+      return fail(PGSR_EINVAL, "sequence id %d outside [0, %d)", s, p->max_seqs);
+    if (seen[s]) return fail(PGSR_EINVAL, "sequence id %d appears twice in one call", s);
+    seen[s] = 1;
+  }
+  return PGSR_OK;
+}
+
+// ------------------------------------------------------------------ crop -- //
+int do_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_lens,
+            unsigned flags, hipStream_t st) {
+  int32_t top = p->h_top;
+  for (int32_t base = 0; base < n; base += kMaxSeqsPerLaunch) {
+    const int32_t cnt = std::min<int32_t>(kMaxSeqsPerLaunch, n - base);
+    CropArgs a{};
+    a.tables = p->tables;
+    a.lens = p->lens;
+    a.free_list = p->free_list;
+    a.free_top = p->free_top;
+    a.max_bps = p->max_bps;
+    a.top_before = top;
+    a.n = cnt;
+    int32_t off = 0;
+    for (int32_t i = 0; i < cnt; ++i) {
+      const int32_t s = seqs[base + i], L = new_lens[base + i];
+      CropEntry& e = a.e[i];
+      e.seq = s;
+      e.new_len = L;
+      e.keep = cdiv(L, p->B);
+      e.nalloc = p->h_nalloc[s];
+      e.push_off = off;
+      off += e.nalloc - e.keep;
+    }
+    a.top_after = top + off;
+    hipError_t err = launch_crop(a, st);
+    if (err != hipSuccess) return hip_fail(err, "crop launch");
+    if (flags & PGSR_POISON) {
+      PoisonArgs pa{};
+      pa.k_cache = p->k_cache;
+      pa.v_cache = p->v_cache;
+      pa.tables = p->tables;
+      pa.free_list = p->free_list;
+      pa.max_bps = p->max_bps;
+      pa.n_layers = p->n_layers;
+      pa.n_blocks = p->n_blocks;
+      pa.n_kv_heads = p->hkv;
+      pa.block_size = p->B;
+      pa.head_dim = p->d;
+      pa.elem_bytes = elem_bytes(p);
+      pa.top_before = top;
+      pa.n = cnt;
+      std::memcpy(pa.e, a.e, sizeof(CropEntry) * cnt);
+      err = launch_poison(pa, st);
+      if (err != hipSuccess) return hip_fail(err, "poison launch");
+    }
+    for (int32_t i = 0; i < cnt; ++i) {
+      p->h_nalloc[a.e[i].seq] = a.e[i].keep;
+      p->h_len[a.e[i].seq] = a.e[i].new_len;
+    }
+    top = a.top_after;
+    p->h_top = top;
+  }
+  return PGSR_OK;
+}
+
+// ---------------------------------------------------------------- replay -- //
+struct Seg {
+  int32_t seq, prefix, q_len, q_off;
+};
+
+// Validation of a replay step: lengths, table width, free blocks.
+int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+                 const int32_t* q_lens, const void* q, const void* k, const void* v,
+                 const void* o, const std::vector<int32_t>& prefix,
+                 const std::vector<int32_t>& nalloc, int32_t free_blocks, float scale) {
+  if (layer < 0 || layer >= p->n_layers)
+    return fail(PGSR_EINVAL, "layer %d outside [0, %d)", layer, p->n_layers);
+  if (!std::isfinite(scale)) return fail(PGSR_EINVAL, "softmax_scale is not finite");
+  int64_t total = 0, need = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t S = q_lens[i];
+    if (S < 0) return fail(PGSR_EINVAL, "q_lens[%d] = %d is negative", i, S);
+    const int64_t end = (int64_t)prefix[i] + S;
+    if (end > (int64_t)p->max_bps * p->B)
+      return fail(PGSR_ERANGE, "sequence %d would reach %lld tokens; its row holds %lld",
+                  seqs[i], (long long)end, (long long)p->max_bps * p->B);
+    need += std::max<int64_t>(0, cdiv(end, p->B) - nalloc[i]);
+    total += S;
+  }
+  if (total > INT32_MAX) return fail(PGSR_ERANGE, "more than 2^31-1 query tokens in one call");
+  if (total > 0 && (!q || !k || !v || !o))
+    return fail(PGSR_EINVAL, "null q/k/v/o pointer with %lld query tokens", (long long)total);
+  if (need > free_blocks)
+    return fail(PGSR_ENOMEM, "step needs %lld free blocks, %d available", (long long)need,
+                free_blocks);
+  return PGSR_OK;
+}
+
+int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+              const int32_t* q_lens, const void* q, const void* k, const void* v, void* o,
+              float scale, unsigned flags, int64_t* recomputed, hipStream_t st) {
+  // Segments with work, in call order (the packed inputs follow call order).
+  std::vector<Seg> segs;
+  segs.reserve(n);
+  int32_t off = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = seqs[i];
+    if (q_lens[i] > 0) segs.push_back({s, p->h_len[s], q_lens[i], off});
+    off += q_lens[i];
+  }
+  const bool commit = (flags & PGSR_COMMIT) != 0;
+  const int eb = elem_bytes(p);
+
+  if (p->timing) {
+    hipError_t err = hipEventRecord(p->ev[0], st);
+    if (err != hipSuccess) return hip_fail(err, "timing event");
+  }
+  // Reserve + append, chunked.
+  int32_t top = p->h_top;
+  for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
+    const int32_t cnt = (int32_t)std::min<size_t>(kMaxSeqsPerLaunch, segs.size() - base);
+    AppendArgs a{};
+    a.k_cache = p->k_cache;
+    a.v_cache = p->v_cache;
+    a.k_in = k;
+    a.v_in = v;
+    a.tables = p->tables;
+    a.lens = p->lens;
+    a.free_list = p->free_list;
+    a.free_top = p->free_top;
+    a.max_bps = p->max_bps;
+    a.n_blocks = p->n_blocks;
+    a.n_kv_heads = p->hkv;
+    a.block_size = p->B;
+    a.head_dim = p->d;
+    a.layer = layer;
+    a.commit = commit ? 1 : 0;
+    a.n = cnt;
+    int32_t items = 0;
+    for (int32_t i = 0; i < cnt; ++i) {
+      const Seg& g = segs[base + i];
+      AppendEntry& e = a.e[i];
+      e.seq = g.seq;
+      e.prefix = g.prefix;
+      e.q_len = g.q_len;
+      e.q_off = g.q_off;
+      e.nalloc_before = p->h_nalloc[g.seq];
+      e.stack_before = top;
+      e.lb_first = g.prefix / p->B;
+      e.item_start = items;
+      const int32_t end_blocks = cdiv((int64_t)g.prefix + g.q_len, p->B);
+      items += end_blocks - e.lb_first;
+      const int32_t pops = std::max(0, end_blocks - e.nalloc_before);
+      top -= pops;
+    }
+    a.n_items = items;
+    a.write_top = 1;
+    a.top_after = top;
+    hipError_t err = launch_append(a, eb, st);
+    if (err != hipSuccess) return hip_fail(err, "append launch");
+    for (int32_t i = 0; i < cnt; ++i) {
+      const Seg& g = segs[base + i];
+      p->h_nalloc[g.seq] =
+          std::max(p->h_nalloc[g.seq], cdiv((int64_t)g.prefix + g.q_len, p->B));
+    }
+    p->h_top = top;
+  }
+
+  if (p->timing) {
+    hipError_t err = hipEventRecord(p->ev[1], st);
+    if (err == hipSuccess) err = hipEventRecord(p->ev[2], st);
+    if (err != hipSuccess) return hip_fail(err, "timing event");
+  }
+  // Attention, chunked; within a launch, costlier sequences first.
+  const int group = p->hq / p->hkv;
+  const int tile_tokens = p->dtype == PGSR_F32 ? attn_f32_tile_tokens(p->d, group)
+                                                : attn_bf16_tile_tokens(p->d, group);
+  for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
+    const int32_t cnt = (int32_t)std::min<size_t>(kMaxSeqsPerLaunch, segs.size() - base);
+    std::vector<Seg> chunk(segs.begin() + base, segs.begin() + base + cnt);
+    std::stable_sort(chunk.begin(), chunk.end(), [](const Seg& x, const Seg& y) {
+      const double cx = (double)x.q_len * (x.prefix + 0.5 * x.q_len);
+      const double cy = (double)y.q_len * (y.prefix + 0.5 * y.q_len);
+      return cx > cy;
+    });
+    AttnArgs a{};
+    a.q = q;
+    a.o = o;
+    a.k_cache = p->k_cache;
+    a.v_cache = p->v_cache;
+    a.tables = p->tables;
+    a.max_bps = p->max_bps;
+    a.n_blocks = p->n_blocks;
+    a.n_q_heads = p->hq;
+    a.n_kv_heads = p->hkv;
+    a.block_size = p->B;
+    a.head_dim = p->d;
+    a.layer = layer;
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    a.n = cnt;
+    int32_t tiles = 0;
+    for (int32_t i = 0; i < cnt; ++i) {
+      a.e[i].seq = chunk[i].seq;
+      a.e[i].prefix = chunk[i].prefix;
+      a.e[i].q_len = chunk[i].q_len;
+      a.e[i].q_off = chunk[i].q_off;
+      a.e[i].tile_start = tiles;
+      tiles += cdiv(chunk[i].q_len, tile_tokens);
+    }
+    a.n_tiles = tiles;
+    hipError_t err = p->dtype == PGSR_F32 ? launch_attn_f32(a, st) : launch_attn_bf16(a, st);
+    if (err != hipSuccess) return hip_fail(err, "attention launch");
+  }
+
+  if (p->timing) {
+    hipError_t err = hipEventRecord(p->ev[3], st);
+    if (err != hipSuccess) return hip_fail(err, "timing event");
+    p->timed_call = true;
+  }
+  if (commit) {
+    int64_t total = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      p->h_len[seqs[i]] += q_lens[i];
+      total += q_lens[i];
+    }
+    if (recomputed) *recomputed += total;
+  }
+  return PGSR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pgsr_last_error(void) { return g_err.c_str(); }
+
+int pgsr_abi_version(void) { return 1; }
+
+int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                     int32_t block_size, int32_t dtype, int32_t n_blocks, int32_t max_seqs,
+                     int32_t max_blocks_per_seq, void* k_cache, void* v_cache,
+                     int32_t* block_tables, int32_t* seq_lens, int32_t* free_list,
+                     int32_t* free_top, void* workspace, size_t workspace_bytes,
+                     const int32_t* init_free_order, void* stream, pgsr_pool** out) {
+  if (!out) return fail(PGSR_EINVAL, "out is null");
+  *out = nullptr;
+  if (n_layers <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_blocks <= 0 || max_seqs <= 0 ||
+      max_blocks_per_seq <= 0)
+    return fail(PGSR_EINVAL, "sizes must be positive");
+  if (n_q_heads % n_kv_heads != 0)
+    return fail(PGSR_EUNSUPPORTED, "n_q_heads %d is not a multiple of n_kv_heads %d", n_q_heads,
+                n_kv_heads);
+  if (dtype != PGSR_F32 && dtype != PGSR_BF16) return fail(PGSR_EUNSUPPORTED, "dtype %d", dtype);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(PGSR_EUNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16 && block_size != 32 && block_size != 64)
+    return fail(PGSR_EUNSUPPORTED, "block_size %d (supported: 16, 32, 64)", block_size);
+  const int group = n_q_heads / n_kv_heads;
+  if (dtype == PGSR_BF16 && (32 % group != 0))
+    return fail(PGSR_EUNSUPPORTED, "bf16 kernels need n_q_heads / n_kv_heads to divide 32");
+  if ((int64_t)max_seqs * max_blocks_per_seq > INT32_MAX)
+    return fail(PGSR_ERANGE, "block table larger than 2^31-1 entries");
+  if (!k_cache || !v_cache || !block_tables || !seq_lens || !free_list || !free_top)
+    return fail(PGSR_EINVAL, "null device pointer");
+  if (workspace == nullptr) workspace_bytes = 0;
+  if (init_free_order) {
+    std::vector<char> seen(n_blocks, 0);
+    for (int32_t i = 0; i < n_blocks; ++i) {
+      const int32_t id = init_free_order[i];
+      if (id < 0 || id >= n_blocks || seen[id])
+        return fail(PGSR_EINVAL, "init_free_order is not a permutation of 0..%d", n_blocks - 1);
+      seen[id] = 1;
+    }
+  }
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t err = launch_pool_init(block_tables, (int64_t)max_seqs * max_blocks_per_seq,
+                                    seq_lens, max_seqs, init_free_order ? nullptr : free_list,
+                                    n_blocks, free_top, st);
+  if (err != hipSuccess) return hip_fail(err, "pool init launch");
+  if (init_free_order) {
+    err = hipMemcpyAsync(free_list, init_free_order, sizeof(int32_t) * n_blocks,
+                         hipMemcpyHostToDevice, st);
+    if (err != hipSuccess) return hip_fail(err, "copy of init_free_order");
+  }
+  err = hipStreamSynchronize(st);
+  if (err != hipSuccess) return hip_fail(err, "pool init");
+  pgsr_pool* p = new pgsr_pool{};
+  p->n_layers = n_layers;
+  p->hq = n_q_heads;
+  p->hkv = n_kv_heads;
+  p->d = head_dim;
+  p->B = block_size;
+  p->dtype = dtype;
+  p->n_blocks = n_blocks;
+  p->max_seqs = max_seqs;
+  p->max_bps = max_blocks_per_seq;
+  p->k_cache = k_cache;
+  p->v_cache = v_cache;
+  p->tables = block_tables;
+  p->lens = seq_lens;
+  p->free_list = free_list;
+  p->free_top = free_top;
+  p->workspace = workspace;
+  p->workspace_bytes = workspace_bytes;
+  p->h_len.assign(max_seqs, 0);
+  p->h_nalloc.assign(max_seqs, 0);
+  p->h_top = n_blocks;
+  *out = p;
+  return ok();
+}
+
+int pgsr_pool_destroy(pgsr_pool* pool) {
+  if (pool)
+    for (hipEvent_t& e : pool->ev)
+      if (e) (void)hipEventDestroy(e);
+  delete pool;
+  return ok();
+}
+
+int pgsr_pool_enable_timing(pgsr_pool* p, int on) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  if (on && !p->ev[0]) {
+    for (hipEvent_t& e : p->ev) {
+      hipError_t err = hipEventCreate(&e);
+      if (err != hipSuccess) return hip_fail(err, "hipEventCreate");
+    }
+  }
+  p->timing = on != 0;
+  p->timed_call = false;
+  return ok();
+}
+
+int pgsr_pool_last_times(pgsr_pool* p, float* append_ms, float* attention_ms) {
+  if (!p || !append_ms || !attention_ms) return fail(PGSR_EINVAL, "null argument");
+  if (!p->timed_call) return fail(PGSR_EINVAL, "no timed call since timing was enabled");
+  hipError_t err = hipEventSynchronize(p->ev[3]);
+  if (err == hipSuccess) err = hipEventElapsedTime(append_ms, p->ev[0], p->ev[1]);
+  if (err == hipSuccess) err = hipEventElapsedTime(attention_ms, p->ev[2], p->ev[3]);
+  if (err != hipSuccess) return hip_fail(err, "event timing");
+  return ok();
+}
+
+int pgsr_pool_refresh(pgsr_pool* p, void* stream) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  hipStream_t st = (hipStream_t)stream;
+  std::vector<int32_t> tables((size_t)p->max_seqs * p->max_bps), lens(p->max_seqs);
+  int32_t top = 0;
+  hipError_t err = hipMemcpyAsync(tables.data(), p->tables, tables.size() * 4,
+                                  hipMemcpyDeviceToHost, st);
+  if (err == hipSuccess)
+    err = hipMemcpyAsync(lens.data(), p->lens, lens.size() * 4, hipMemcpyDeviceToHost, st);
+  if (err == hipSuccess) err = hipMemcpyAsync(&top, p->free_top, 4, hipMemcpyDeviceToHost, st);
+  if (err == hipSuccess) err = hipStreamSynchronize(st);
+  if (err != hipSuccess) return hip_fail(err, "refresh copy");
+  if (top < 0 || top > p->n_blocks) return fail(PGSR_ERANGE, "device free_top %d invalid", top);
+  for (int32_t s = 0; s < p->max_seqs; ++s) {
+    int32_t na = 0;
+    while (na < p->max_bps && tables[(size_t)s * p->max_bps + na] >= 0) ++na;
+    if (lens[s] < 0 || cdiv(lens[s], p->B) > na)
+      return fail(PGSR_ERANGE, "device length %d of sequence %d exceeds its blocks", lens[s], s);
+    p->h_nalloc[s] = na;
+    p->h_len[s] = lens[s];
+  }
+  p->h_top = top;
+  return ok();
+}
+
+int pgsr_seq_len(const pgsr_pool* p, int32_t seq, int32_t* len_out) {
+  if (!p || !len_out) return fail(PGSR_EINVAL, "null argument");
+  if (seq < 0 || seq >= p->max_seqs) return fail(PGSR_EINVAL, "sequence id %d", seq);
+  *len_out = p->h_len[seq];
+  return ok();
+}
+
+int pgsr_free_blocks(const pgsr_pool* p, int32_t* n_out) {
+  if (!p || !n_out) return fail(PGSR_EINVAL, "null argument");
+  *n_out = p->h_top;
+  return ok();
+}
+
+size_t pgsr_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int64_t max_total_q,
+                            int32_t max_splits) {
+  if (n_q_heads <= 0 || head_dim <= 0 || max_total_q <= 0 || max_splits <= 1) return 0;
+  return (size_t)max_total_q * n_q_heads * max_splits * ((size_t)head_dim + 2) * sizeof(float);
+}
+
+int pgsr_kv_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_lens,
+                 unsigned flags, void* stream) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
+  if (n == 0) return ok();
+  if (!seqs || !new_lens) return fail(PGSR_EINVAL, "null seqs / new_lens");
+  if (flags & ~(unsigned)PGSR_POISON) return fail(PGSR_EINVAL, "unknown crop flags 0x%x", flags);
+  int rc = check_seqs(p, n, seqs);
+  if (rc) return rc;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t L = new_lens[i], len = p->h_len[seqs[i]];
+    if (L < 0 || L > len)
+      return fail(PGSR_ERANGE, "crop of sequence %d to %d tokens; it holds %d", seqs[i], L, len);
+  }
+  rc = do_crop(p, n, seqs, new_lens, flags, (hipStream_t)stream);
+  return rc ? rc : ok();
+}
+
+int pgsr_replay_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+                        const int32_t* q_lens, const void* q, const void* k, const void* v,
+                        void* o, float softmax_scale, unsigned flags,
+                        int64_t* recomputed_tokens, void* stream) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
+  if (flags & ~(unsigned)PGSR_COMMIT) return fail(PGSR_EINVAL, "unknown replay flags 0x%x", flags);
+  if (n > 0 && (!seqs || !q_lens)) return fail(PGSR_EINVAL, "null seqs / q_lens");
+  int rc = check_seqs(p, n, seqs);
+  if (rc) return rc;
+  std::vector<int32_t> prefix(n), nalloc(n);
+  for (int32_t i = 0; i < n; ++i) {
+    prefix[i] = p->h_len[seqs[i]];
+    nalloc[i] = p->h_nalloc[seqs[i]];
+  }
+  rc = check_replay(p, layer, n, seqs, q_lens, q, k, v, o, prefix, nalloc, p->h_top,
+                    softmax_scale);
+  if (rc) return rc;
+  rc = do_replay(p, layer, n, seqs, q_lens, q, k, v, o, softmax_scale, flags, recomputed_tokens,
+                 (hipStream_t)stream);
+  return rc ? rc : ok();
+}
+
+int pgsr_full_reset_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+                            const int32_t* lens, const void* q, const void* k, const void* v,
+                            void* o, float softmax_scale, unsigned flags,
+                            int64_t* recomputed_tokens, void* stream) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
+  if (flags & ~(unsigned)PGSR_COMMIT) return fail(PGSR_EINVAL, "unknown replay flags 0x%x", flags);
+  if (n > 0 && (!seqs || !lens)) return fail(PGSR_EINVAL, "null seqs / lens");
+  int rc = check_seqs(p, n, seqs);
+  if (rc) return rc;
+  // Validate the replay as it will run after the crop (prefix 0, rows emptied).
+  std::vector<int32_t> prefix(n), nalloc(n);
+  int32_t free_after = p->h_top;
+  for (int32_t i = 0; i < n; ++i) {
+    if (layer == 0) {
+      prefix[i] = 0;
+      nalloc[i] = 0;
+      free_after += p->h_nalloc[seqs[i]];
+    } else {
+      prefix[i] = p->h_len[seqs[i]];
+      nalloc[i] = p->h_nalloc[seqs[i]];
+    }
+  }
+  rc = check_replay(p, layer, n, seqs, lens, q, k, v, o, prefix, nalloc, free_after,
+                    softmax_scale);
+  if (rc) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  if (layer == 0 && n > 0) {
+    std::vector<int32_t> zeros(n, 0);
+    rc = do_crop(p, n, seqs, zeros.data(), 0, st);
+    if (rc) return rc;
+  }
+  rc = do_replay(p, layer, n, seqs, lens, q, k, v, o, softmax_scale, flags, recomputed_tokens, st);
+  return rc ? rc : ok();
+}
+
+int pgsr_gemm_bf16(int32_t m, int32_t n, int32_t k, const void* x, const void* w, const void* r,
+                   void* y, void* stream) {
+  if (m < 0 || n < 0 || k < 0) return fail(PGSR_EINVAL, "negative size");
+  if (n % 8 || k % 8) return fail(PGSR_EUNSUPPORTED, "n and k must be multiples of 8");
+  if (m == 0 || n == 0) return ok();
+  if (!x || !w || !y) return fail(PGSR_EINVAL, "null pointer");
+  hipError_t err = launch_gemm_bf16(m, n, k, x, w, r, y, (hipStream_t)stream);
+  if (err != hipSuccess) return hip_fail(err, "gemm launch");
+  return ok();
+}
+
+}  // extern "C"

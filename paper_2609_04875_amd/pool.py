@@ -1,0 +1,152 @@
+"""Paged KV pool over torch device memory, driving the C ABI.
+
+``KVPool`` allocates the caller-owned device arrays the library works on
+(caches, block table, lengths, free-list stack, split workspace) and exposes
+the three calls of the hot path: ``crop`` (restore, Algorithm 1), ``replay``
+(the prefill form of the replay loop) and ``full_reset`` (baseline B5).
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Sequence
+
+import torch
+
+from . import _native as N
+
+_DT = {N.F32: torch.float32, N.BF16: torch.bfloat16}
+
+
+def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> Optional[int]:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream or None
+
+
+def _dev_ptr(t: Optional[torch.Tensor], dtype, name: str) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous() or t.dtype != dtype:
+        raise ValueError(f"{name} must be a contiguous {dtype} CUDA tensor")
+    return t.data_ptr() if t.numel() else None
+
+
+class KVPool:
+    def __init__(self, n_layers: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                 n_blocks: int, max_seqs: int, max_blocks_per_seq: int, dtype: int = N.BF16,
+                 block_size: int = 16, init_free_order: Optional[Sequence[int]] = None,
+                 workspace_bytes: int = 0, device: str = "cuda",
+                 stream: Optional[torch.cuda.Stream] = None):
+        self.n_layers, self.hq, self.hkv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
+        self.n_blocks, self.max_seqs, self.max_bps = n_blocks, max_seqs, max_blocks_per_seq
+        self.B, self.dtype_code = block_size, dtype
+        self.dtype = _DT[dtype]
+        shape = (n_layers, n_blocks, n_kv_heads, block_size, head_dim)
+        self.k_cache = torch.zeros(shape, dtype=self.dtype, device=device)
+        self.v_cache = torch.zeros((n_layers, n_blocks, n_kv_heads, head_dim, block_size),
+                                   dtype=self.dtype, device=device)
+        self.block_tables = torch.empty((max_seqs, max_blocks_per_seq), dtype=torch.int32, device=device)
+        self.seq_lens = torch.empty((max_seqs,), dtype=torch.int32, device=device)
+        self.free_list = torch.empty((n_blocks,), dtype=torch.int32, device=device)
+        self.free_top = torch.empty((1,), dtype=torch.int32, device=device)
+        self.workspace = (torch.empty((workspace_bytes,), dtype=torch.uint8, device=device)
+                          if workspace_bytes else None)
+        order = N.int32_array(init_free_order) if init_free_order is not None else None
+        handle = ctypes.c_void_p()
+        N.check(N.lib.pgsr_pool_create(
+            n_layers, n_q_heads, n_kv_heads, head_dim, block_size, dtype, n_blocks, max_seqs,
+            max_blocks_per_seq, self.k_cache.data_ptr(), self.v_cache.data_ptr(),
+            self.block_tables.data_ptr(), self.seq_lens.data_ptr(), self.free_list.data_ptr(),
+            self.free_top.data_ptr(),
+            self.workspace.data_ptr() if self.workspace is not None else None,
+            workspace_bytes, order, _stream_ptr(stream), ctypes.byref(handle)))
+        self._h = handle
+        self.recomputed_tokens = ctypes.c_int64(0)
+
+    def close(self) -> None:
+        if self._h:
+            N.lib.pgsr_pool_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---- host-mirror queries ----
+    def seq_len(self, seq: int) -> int:
+        out = ctypes.c_int32()
+        N.check(N.lib.pgsr_seq_len(self._h, seq, ctypes.byref(out)))
+        return out.value
+
+    def free_blocks(self) -> int:
+        out = ctypes.c_int32()
+        N.check(N.lib.pgsr_free_blocks(self._h, ctypes.byref(out)))
+        return out.value
+
+    def refresh(self, stream=None) -> None:
+        N.check(N.lib.pgsr_pool_refresh(self._h, _stream_ptr(stream)))
+
+    # ---- kernel timing (HIP events recorded by the library on the call's stream) ----
+    def enable_timing(self, on: bool = True) -> None:
+        N.check(N.lib.pgsr_pool_enable_timing(self._h, 1 if on else 0))
+
+    def last_times(self):
+        """(append_ms, attention_ms) of the most recent replay / full-reset call."""
+        a, b = ctypes.c_float(), ctypes.c_float()
+        N.check(N.lib.pgsr_pool_last_times(self._h, ctypes.byref(a), ctypes.byref(b)))
+        return a.value, b.value
+
+    # ---- the hot path ----
+    def crop(self, seqs: Sequence[int], new_lens: Sequence[int], poison: bool = False,
+             stream=None) -> int:
+        """Restore = crop; returns the status (0 ok) instead of raising."""
+        return N.lib.pgsr_kv_crop(self._h, len(seqs), N.int32_array(seqs), N.int32_array(new_lens),
+                                  N.POISON if poison else 0, _stream_ptr(stream))
+
+    def _prefill(self, fn, layer, seqs, q_lens, q, k, v, o, scale, commit, stream) -> int:
+        dt = self.dtype
+        return fn(self._h, layer, len(seqs), N.int32_array(seqs), N.int32_array(q_lens),
+                  _dev_ptr(q, dt, "q"), _dev_ptr(k, dt, "k"), _dev_ptr(v, dt, "v"),
+                  _dev_ptr(o, dt, "o"), float(scale), N.COMMIT if commit else 0,
+                  ctypes.byref(self.recomputed_tokens), _stream_ptr(stream))
+
+    def replay(self, layer: int, seqs, q_lens, q, k, v, o, scale: float, commit: bool = True,
+               stream=None) -> int:
+        return self._prefill(N.lib.pgsr_replay_prefill, layer, seqs, q_lens, q, k, v, o, scale,
+                             commit, stream)
+
+    def full_reset(self, layer: int, seqs, lens, q, k, v, o, scale: float, commit: bool = True,
+                   stream=None) -> int:
+        return self._prefill(N.lib.pgsr_full_reset_prefill, layer, seqs, lens, q, k, v, o, scale,
+                             commit, stream)
+
+    # ---- state snapshots (device -> host), for tests and the benchmark ----
+    def state(self):
+        torch.cuda.synchronize()
+        return {"tables": self.block_tables.cpu().numpy(), "lens": self.seq_lens.cpu().numpy(),
+                "free": self.free_list.cpu().numpy(), "top": int(self.free_top.item())}
+
+    def save_meta(self):
+        return [t.clone() for t in (self.block_tables, self.seq_lens, self.free_list, self.free_top)]
+
+    def load_meta(self, saved) -> None:
+        for dst, src in zip((self.block_tables, self.seq_lens, self.free_list, self.free_top), saved):
+            dst.copy_(src)
+        self.refresh()
+
+
+def gemm_bf16(x: torch.Tensor, w: torch.Tensor, r: Optional[torch.Tensor] = None,
+              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Y = X W (+ R) on the library's MFMA GEMM; bf16 in and out, fp32 accumulation."""
+    m, k = x.shape
+    k2, n = w.shape
+    if k2 != k:
+        raise ValueError("inner dimensions differ")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.bfloat16, device=x.device)
+    N.check(N.lib.pgsr_gemm_bf16(m, n, k, _dev_ptr(x, torch.bfloat16, "x"),
+                                 _dev_ptr(w, torch.bfloat16, "w"),
+                                 _dev_ptr(r, torch.bfloat16, "r") if r is not None else None,
+                                 _dev_ptr(out, torch.bfloat16, "out"), _stream_ptr(stream)))
+    return out

@@ -1,0 +1,73 @@
+"""The C ABI library loads and exports every symbol include/pgsr.h declares;
+host-side validation answers without touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pgsr.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pgsr_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def native():
+    from paper_2609_04875_amd import _native
+    return _native
+
+
+def test_header_declares_the_hot_path():
+    names = declared_functions()
+    for must in ("pgsr_kv_crop", "pgsr_replay_prefill", "pgsr_full_reset_prefill"):
+        assert must in names
+
+
+def test_every_declared_symbol_is_exported(native):
+    names = declared_functions()
+    raw = ctypes.CDLL(native.LIB_PATH)
+    missing = [n for n in names if not hasattr(raw, n)]
+    assert not missing, missing
+    assert set(names) == set(native.EXPORTS)
+
+
+def test_abi_version_and_workspace_size(native):
+    assert native.lib.pgsr_abi_version() == 1
+    assert native.lib.pgsr_workspace_bytes(32, 128, 2048, 4) == 2048 * 32 * 4 * 130 * 4
+    assert native.lib.pgsr_workspace_bytes(32, 128, 2048, 1) == 0
+
+
+def test_create_rejects_bad_geometry_before_any_device_call(native):
+    out = ctypes.c_void_p()
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    args = dict(n_layers=1, hq=32, hkv=8, d=128, B=16, dt=native.BF16, nb=64, ms=2, mbps=8)
+
+    def create(**kw):
+        a = {**args, **kw}
+        return native.lib.pgsr_pool_create(a["n_layers"], a["hq"], a["hkv"], a["d"], a["B"], a["dt"],
+                                           a["nb"], a["ms"], a["mbps"], fake, fake, fake, fake, fake,
+                                           fake, None, 0, None, None, ctypes.byref(out))
+    assert create(d=96) == native.EUNSUPPORTED
+    assert create(B=8) == native.EUNSUPPORTED
+    assert create(hq=30) == native.EUNSUPPORTED
+    assert create(hq=24, hkv=8) == native.EUNSUPPORTED       # group 3 does not divide 32 (bf16)
+    assert create(dt=7) == native.EUNSUPPORTED
+    assert create(nb=0) == native.EINVAL
+    order = native.int32_array([0, 1, 1] + list(range(3, 64)))
+    assert native.lib.pgsr_pool_create(1, 32, 8, 128, 16, native.BF16, 64, 2, 8, fake, fake, fake,
+                                       fake, fake, fake, None, 0, order, None,
+                                       ctypes.byref(out)) == native.EINVAL
+    assert b"permutation" in native.lib.pgsr_last_error()
+    assert not out.value
+
+
+def test_null_pool_and_gemm_validation(native):
+    assert native.lib.pgsr_kv_crop(None, 0, None, None, 0, None) == native.EINVAL
+    assert native.lib.pgsr_gemm_bf16(4, 12, 16, None, None, None, None, None) == native.EUNSUPPORTED
+    assert native.lib.pgsr_gemm_bf16(0, 16, 16, None, None, None, None, None) == native.OK
+    assert native.lib.pgsr_gemm_bf16(4, 16, 16, None, None, None, None, None) == native.EINVAL

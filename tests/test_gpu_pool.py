@@ -1,0 +1,154 @@
+"""GPU parity of restore-by-crop and reserve+append against the oracle's pool
+model: block tables, lengths, free-list stack and stack height bit-exact after
+every call (Algorithm 1 restore and replay steps; Section 3.4 (b)), appended
+K/V bits exact, kept prefix untouched (Lemma 1), errors change nothing."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from gpu_helpers import bits, dev, log, logical_kv, make_pool
+
+pytestmark = pytest.mark.gpu
+
+GEOM = W.AttnGeometry(8, 2, 64)
+
+
+def _compare(pool, model, where):
+    st = pool.state()
+    np.testing.assert_array_equal(st["tables"], model.tables, err_msg=where)
+    np.testing.assert_array_equal(st["lens"], model.lens, err_msg=where)
+    np.testing.assert_array_equal(st["free"], model.free, err_msg=where)
+    assert st["top"] == model.top, where
+
+
+@pytest.mark.parametrize("dtype,B,seed", [("bf16", 16, 0), ("f32", 16, 1), ("bf16", 32, 2), ("bf16", 64, 3)])
+def test_random_crop_replay_trace_matches_oracle(dtype, B, seed):
+    log(f"trace dtype={dtype} B={B} seed={seed}")
+    rng = np.random.default_rng(seed)
+    n_seqs, max_bps = 5, 24
+    nb = 70
+    order = rng.permutation(nb).tolist()
+    pool = make_pool(GEOM, dtype, nb, n_seqs, max_bps, block_size=B, init_free_order=order)
+    model = oracle.PoolModel(nb, n_seqs, max_bps, B, init_free_order=order)
+    store_dt = np.float32 if dtype == "f32" else np.uint16
+    expect_k = [np.zeros((0, GEOM.n_kv_heads, GEOM.head_dim), store_dt) for _ in range(n_seqs)]
+    expect_v = [x.copy() for x in expect_k]
+    _compare(pool, model, "init")
+    for step in range(40):
+        if rng.random() < 0.45:
+            seqs = rng.choice(n_seqs, size=int(rng.integers(1, 4)), replace=False).tolist()
+            new = [int(rng.integers(0, model.lens[s] + 1)) for s in seqs]
+            if rng.random() < 0.1:                       # an invalid crop: nothing may change
+                new[0] = int(model.lens[seqs[0]]) + 1
+            want = model.crop(seqs, new)
+            got = pool.crop(seqs, new)
+            assert got == want, (step, got, want)
+            if want == 0:
+                for s, L in zip(seqs, new):
+                    expect_k[s], expect_v[s] = expect_k[s][:L], expect_v[s][:L]
+        else:
+            seqs = rng.choice(n_seqs, size=int(rng.integers(1, 4)), replace=False).tolist()
+            q_lens = [int(rng.integers(0, 3 * B)) for _ in seqs]
+            tot = sum(q_lens)
+            q = rng.standard_normal((tot, GEOM.n_q_heads, GEOM.head_dim)).astype(np.float32)
+            k = rng.standard_normal((tot, GEOM.n_kv_heads, GEOM.head_dim)).astype(np.float32)
+            v = rng.standard_normal((tot, GEOM.n_kv_heads, GEOM.head_dim)).astype(np.float32)
+            q, k, v = (W.round_to_dtype(x, dtype) for x in (q, k, v))
+            o = torch.empty((tot, GEOM.n_q_heads, GEOM.head_dim), dtype=pool.dtype, device="cuda")
+            want = model.reserve(seqs, q_lens)
+            got = pool.replay(0, seqs, q_lens, dev(q, dtype), dev(k, dtype), dev(v, dtype), o, 0.125)
+            assert got == want, (step, got, want)
+            if want == 0:
+                model.commit(seqs, q_lens)
+                off = 0
+                for s, S in zip(seqs, q_lens):
+                    expect_k[s] = np.concatenate([expect_k[s], k[off:off + S]])
+                    expect_v[s] = np.concatenate([expect_v[s], v[off:off + S]])
+                    off += S
+        _compare(pool, model, f"step {step}")
+        for s in range(n_seqs):
+            assert pool.seq_len(s) == model.lens[s]
+            n = int(model.lens[s])
+            if n:
+                kk, vv = logical_kv(pool, 0, s, n)
+                np.testing.assert_array_equal(bits(kk), np.ascontiguousarray(expect_k[s]).view(bits(kk).dtype))
+                np.testing.assert_array_equal(bits(vv), np.ascontiguousarray(expect_v[s]).view(bits(vv).dtype))
+    assert pool.free_blocks() == model.top
+
+
+def test_crop_of_many_sequences_in_one_call():
+    # more sequences than one launch carries: the launches split, order kept
+    n_seqs, B, nb = 150, 16, 600
+    pool = make_pool(GEOM, "bf16", nb, n_seqs, 8, block_size=B)
+    model = oracle.PoolModel(nb, n_seqs, 8, B)
+    rng = np.random.default_rng(7)
+    seqs = list(range(n_seqs))
+    lens = rng.integers(1, 60, size=n_seqs).tolist()
+    tot = sum(lens)
+    x = W.round_to_dtype(rng.standard_normal((tot, 8, 64)).astype(np.float32), "bf16")
+    kv = W.round_to_dtype(rng.standard_normal((tot, 2, 64)).astype(np.float32), "bf16")
+    o = torch.empty((tot, 8, 64), dtype=torch.bfloat16, device="cuda")
+    assert pool.replay(0, seqs, lens, dev(x, "bf16"), dev(kv, "bf16"), dev(kv, "bf16"), o, 0.1) == 0
+    assert model.reserve(seqs, lens) == 0
+    model.commit(seqs, lens)
+    order = rng.permutation(n_seqs).tolist()
+    new = [int(rng.integers(0, lens[s] + 1)) for s in order]
+    assert pool.crop(order, new) == model.crop(order, new) == 0
+    _compare(pool, model, "after crop")
+
+
+@pytest.mark.parametrize("case", ["dup", "range", "nomem", "width", "badseq"])
+def test_rejected_calls_leave_device_state_unchanged(case):
+    pool = make_pool(GEOM, "bf16", 6, 3, 4)
+    q = torch.randn((200, 8, 64), device="cuda").to(torch.bfloat16)
+    kv = torch.randn((200, 2, 64), device="cuda").to(torch.bfloat16)
+    o = torch.empty_like(q)
+    assert pool.replay(0, [0, 1], [40, 20], q[:60], kv[:60], kv[:60], o[:60], 0.1) == 0
+    before = pool.state()
+    k_before = pool.k_cache.clone()
+    from paper_2609_04875_amd import EINVAL, ERANGE, ENOMEM
+    if case == "dup":
+        assert pool.crop([1, 1], [0, 0]) == EINVAL
+    elif case == "range":
+        assert pool.crop([0], [41]) == ERANGE
+    elif case == "nomem":
+        assert pool.replay(0, [2], [40], q[:40], kv[:40], kv[:40], o[:40], 0.1) == ENOMEM
+    elif case == "width":
+        assert pool.replay(0, [0], [30], q[:30], kv[:30], kv[:30], o[:30], 0.1) == ERANGE
+    elif case == "badseq":
+        assert pool.replay(0, [3], [1], q[:1], kv[:1], kv[:1], o[:1], 0.1) == EINVAL
+    after = pool.state()
+    for key in ("tables", "lens", "free"):
+        np.testing.assert_array_equal(before[key], after[key])
+    assert before["top"] == after["top"]
+    assert torch.equal(pool.k_cache, k_before)
+
+
+def test_poisoned_slots_are_never_read():
+    # After a poisoned crop every released slot is NaN; the replay must still
+    # match the oracle, so no kernel reads past a sequence's length.
+    from gpu_helpers import assert_close, oracle_suffix, storage_f64
+    geom = W.AttnGeometry(32, 8, 128)
+    rng = np.random.default_rng(11)
+    ep = W.draw_episode(rng, geom, "bf16", prefix=109, suffix=70, t_contaminated=300)
+    pool = make_pool(geom, "bf16", 40, 1, 32)
+    from gpu_helpers import contaminated_then_crop
+    contaminated_then_crop(pool, ep, 0, 128 ** -0.5, poison=True)
+    torch.cuda.synchronize()
+    tables = pool.block_tables[0].cpu().numpy()
+    tail_blk = tables[109 // 16]
+    assert torch.isnan(pool.k_cache[0, tail_blk, :, 109 % 16:, :].float()).all()
+    assert torch.isnan(pool.v_cache[0, tail_blk, :, :, 109 % 16:].float()).all()
+    free = pool.state()
+    n_freed = -(-300 // 16) - (-(-109 // 16))
+    freed = free["free"][free["top"] - n_freed: free["top"]]
+    for b in freed:
+        assert torch.isnan(pool.k_cache[0, int(b)].float()).all()
+    q, k, v = (dev(getattr(ep, x)[ep.prefix:], "bf16") for x in ("q", "k", "v"))
+    o = torch.empty_like(q)
+    assert pool.replay(0, [0], [ep.suffix], q, k, v, o, 128 ** -0.5) == 0
+    got = o.float().cpu().numpy()
+    assert np.isfinite(got).all()
+    assert_close(got, oracle_suffix(ep, 128 ** -0.5), "bf16", "poisoned replay")
