@@ -54,7 +54,15 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kNW = 4;   // waves per workgroup
 constexpr int kKT = 64;  // keys per tile
 
-__device__ inline float xor32(float x) { return __shfl_xor(x, 32, 64); }
+// Value of the lane 32 apart (same query row, other half of the wave):
+// v_permlane32_swap exchanges the upper half of its first operand with the
+// lower half of its second, so with both operands = x the low lanes find the
+// partner's x in the second result and the high lanes in the first.
+__device__ inline float xor32(float x) {
+  const int xi = __builtin_bit_cast(int, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(xi, xi, false, false);
+  return __builtin_bit_cast(float, (threadIdx.x & 32) ? r[0] : r[1]);
+}
 
 // Zero 16-bit elements e (0..7) of a 16-byte chunk for which pos0 + e >= limit.
 __device__ inline u32x4 zero_tail(u32x4 v, int pos0, int limit) {
@@ -70,15 +78,19 @@ __device__ inline u32x4 zero_tail(u32x4 v, int pos0, int limit) {
   return v;
 }
 
-template <int D, int NW>
-__global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
+template <int D, int NW, int B>
+__global__ void __launch_bounds__(NW * 64, (NW == 4 ? 2 : 1))
+attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t* __restrict__ qg_,
+                 const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+                 uint16_t* __restrict__ og) {
   constexpr int KT = kKT;
-  constexpr int KLD = D + 8;    // LDS row stride of the K tile (elements)
-  constexpr int VLD = KT + 8;   // LDS row stride of the V^T tile (elements)
+  constexpr int KB = KT / B;               // blocks per key tile
+  constexpr int KLD = D + 8;               // LDS row stride of the K tile (elements)
+  constexpr int VLD = KT + 8;              // LDS row stride of the V^T tile (elements)
   constexpr int NT = NW * 64;
-  constexpr int KCH = KT * D / 8 / NT;  // 16-byte K chunks per thread per tile
-  constexpr int VCH = D * KT / 8 / NT;  // 16-byte V chunks per thread per tile
-  static_assert(KCH * NT * 8 == KT * D && VCH * NT * 8 == KT * D, "tile split");
+  constexpr int CHB = B * D / 8;           // 16-byte chunks per block-head (K or V)
+  constexpr int CPT = KT * D / 8 / NT;     // chunks per thread per tile (K or V)
+  static_assert(CPT * NT * 8 == KT * D, "tile split");
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][KT * KLD];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][D * VLD];
 
@@ -109,8 +121,7 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
   // Q^T operand: lane holds Q[row][16*ds + 8*hh .. +7] for each ds.
   bf16x8 qb[D / 16];
   {
-    const uint16_t* qg =
-        (const uint16_t*)a.q + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 8 * hh;
+    const uint16_t* qg = qg_ + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 8 * hh;
 #pragma unroll
     for (int ds = 0; ds < D / 16; ++ds) {
       u32x4 raw = valid ? *(const u32x4*)(qg + 16 * ds) : u32x4{0, 0, 0, 0};
@@ -118,59 +129,71 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
     }
   }
 
-  const int B = a.block_size;
-  const int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
+  const int32_t* __restrict__ row = tables + (int64_t)e.seq * a.max_bps;
   const int64_t head_base = (int64_t)a.layer * a.n_blocks * hkv + g;  // + id * hkv
-  const uint16_t* kc = (const uint16_t*)a.k_cache;
-  const uint16_t* vc = (const uint16_t*)a.v_cache;
-  const int cpb = B / 8;  // 16-byte chunks per V^T row of one block
+  const int last_blk = (kv_len - 1) / B;   // blocks past it are clamped to it
 
-  u32x4 kreg[KCH], vreg[VCH];
-  auto load_tile = [&](int kb) {
+  // Tile chunking.  A tile is KB block-heads of CHB 16-byte chunks each (K:
+  // (slot, 8 columns); V^T: (d, 8 slots)); thread tid takes chunks
+  // tid + i * NT.  When a block-head has at least NT chunks the block of chunk
+  // i is a compile-time constant, otherwise it depends on tid.
+  constexpr bool kBlkConst = CHB % NT == 0;
+  auto chunk_blk = [&](int i) {
+    if constexpr (kBlkConst) return i / (CHB / NT);
+    else return i * (NT / CHB) + tid / CHB;
+  };
+  auto chunk_in = [&](int i) {
+    if constexpr (kBlkConst) return tid + (i % (CHB / NT)) * NT;
+    else return tid % CHB;
+  };
+
+  // Block ids of a key tile, clamped in range so every tile load is
+  // unconditional (out-of-range keys are masked later).  They are fetched two
+  // tiles ahead as a per-lane vector load (lane bi holds block bi's id; the
+  // vector-memory counter is in order, so waiting for a tile's data never waits
+  // on this), then broadcast to scalar registers with readlane.
+  int32_t ids[KB] = {}, idv = 0;
+  auto fetch_ids = [&](int kb) {
+    idv = row[min(kb / B + (lane < KB ? lane : 0), last_blk)];
+  };
+  auto take_ids = [&]() {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + i * NT;
-      const int key = c / (D / 8), col = c % (D / 8);
-      const int pos = kb + key;
-      u32x4 val = {0, 0, 0, 0};
-      if (pos < kv_len) {
-        const int32_t id = row[pos / B];
-        val = *(const u32x4*)(kc + ((head_base + (int64_t)id * hkv) * B + pos % B) * D + col * 8);
-      }
-      kreg[i] = val;
-    }
+    for (int bi = 0; bi < KB; ++bi) ids[bi] = __builtin_amdgcn_readlane(idv, bi);
+  };
+  auto block_id = [&](int blk) {
+    int32_t id = ids[0];
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = tid + i * NT;
-      const int bi = c / (D * cpb), rem = c % (D * cpb);
-      const int dd = rem / cpb, ck = rem % cpb;
-      const int pos0 = kb + bi * B + ck * 8;
-      u32x4 val = {0, 0, 0, 0};
-      if (pos0 < kv_len) {
-        const int32_t id = row[pos0 / B];
-        val = *(const u32x4*)(vc + ((head_base + (int64_t)id * hkv) * D + dd) * B + pos0 % B);
-        if (pos0 + 8 > kv_len) val = zero_tail(val, pos0, kv_len);
-      }
-      vreg[i] = val;
+    for (int bi = 1; bi < KB; ++bi) id = blk == bi ? ids[bi] : id;
+    return id;
+  };
+
+  u32x4 kreg[CPT], vreg[CPT];
+  auto load_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int blk = chunk_blk(i), in = chunk_in(i);
+      const int64_t base = (head_base + (int64_t)block_id(blk) * hkv) * (B * D);
+      kreg[i] = *(const u32x4*)(kc + base + (in / (D / 8)) * D + (in % (D / 8)) * 8);
+      vreg[i] = *(const u32x4*)(vc + base + (in / (B / 8)) * B + (in % (B / 8)) * 8);
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, int kb) {
+    const bool tail = kb + KT > kv_len;   // V slots at or past kv_len must read as 0
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + i * NT;
-      const int key = c / (D / 8), col = c % (D / 8);
-      *(u32x4*)&k_lds[buf][key * KLD + col * 8] = kreg[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = tid + i * NT;
-      const int bi = c / (D * cpb), rem = c % (D * cpb);
-      const int dd = rem / cpb, ck = rem % cpb;
-      const int key0 = bi * B + ck * 8;            // tile-relative, multiple of 8
+    for (int i = 0; i < CPT; ++i) {
+      const int blk = chunk_blk(i), in = chunk_in(i);
+      *(u32x4*)&k_lds[buf][(blk * B + in / (D / 8)) * KLD + (in % (D / 8)) * 8] = kreg[i];
+      const int dd = in / (B / 8), key0 = blk * B + (in % (B / 8)) * 8;
+      u32x4 val = vreg[i];
+      if (tail) {
+        const int pos0 = kb + key0;
+        if (pos0 >= kv_len) val = u32x4{0, 0, 0, 0};
+        else if (pos0 + 8 > kv_len) val = zero_tail(val, pos0, kv_len);
+      }
       const int base = dd * VLD + (key0 & ~15);
-      const int half = (key0 >> 3) & 1;            // 4-key chunks 2h, 2h+1 -> slots h, h+2
-      *(u32x2*)&v_lds[buf][base + 4 * half] = u32x2{vreg[i][0], vreg[i][1]};
-      *(u32x2*)&v_lds[buf][base + 4 * half + 8] = u32x2{vreg[i][2], vreg[i][3]};
+      const int half = (key0 >> 3) & 1;          // 4-key chunks 2h, 2h+1 -> slots h, h+2
+      *(u32x2*)&v_lds[buf][base + 4 * half] = u32x2{val[0], val[1]};
+      *(u32x2*)&v_lds[buf][base + 4 * half + 8] = u32x2{val[2], val[3]};
     }
   };
 
@@ -180,25 +203,30 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
   float m = -INFINITY, l = 0.f;
   const float c2 = a.scale_log2;
 
-  load_tile(0);
+  fetch_ids(0);
+  take_ids();
+  load_tile();
+  if (n_kt > 1) fetch_ids(KT);
   for (int kt = 0; kt < n_kt; ++kt) {
     const int buf = kt & 1;
     const int kb = kt * KT;
-    store_tile(buf);
+    store_tile(buf, kb);
     __syncthreads();
-    if (kt + 1 < n_kt) load_tile(kb + KT);
+    if (kt + 1 < n_kt) {
+      take_ids();                                  // fetched one tile ago
+      load_tile();                                 // tile kt+1
+      if (kt + 2 < n_kt) fetch_ids(kb + 2 * KT);
+    }
 
-    // S^T = K Q^T for keys kb .. kb+63 (two 32-key halves).
-    f32x16 s[2];
+    // S^T = K Q^T for keys kb .. kb+63: two independent 32-key accumulators.
+    f32x16 s[2] = {f32x16{}, f32x16{}};
+    const uint16_t* kp = &k_lds[buf][r * KLD + 8 * hh];
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {
-      s[kh] = f32x16{};
-      const uint16_t* kp = &k_lds[buf][(kh * 32 + r) * KLD + 8 * hh];
-#pragma unroll
-      for (int ds = 0; ds < D / 16; ++ds) {
-        bf16x8 ka = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 16 * ds));
-        s[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[ds], s[kh], 0, 0, 0);
-      }
+    for (int ds = 0; ds < D / 16; ++ds) {
+      const bf16x8 k0 = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 16 * ds));
+      const bf16x8 k1 = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 32 * KLD + 16 * ds));
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[ds], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[ds], s[1], 0, 0, 0);
     }
     // Causal mask (select) where some key may lie past some row's position.
     if (kb + KT - 1 > first_q) {
@@ -253,7 +281,7 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
   const float l_tot = l + xor32(l);
   if (valid) {
     const float inv = 1.f / l_tot;
-    uint16_t* op = (uint16_t*)a.o + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 4 * hh;
+    uint16_t* op = og + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 4 * hh;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -269,16 +297,30 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
 
 int attn_bf16_tile_tokens(int, int group) { return kNW * 32 / group; }
 
+template <int D, int B>
+static void launch_d_b(const AttnArgs& a, hipStream_t s) {
+  dim3 grid(a.n_tiles * a.n_kv_heads);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, kNW, B>), grid, dim3(kNW * 64), 0, s, a, a.tables,
+                     (const uint16_t*)a.q, (const uint16_t*)a.k_cache,
+                     (const uint16_t*)a.v_cache, (uint16_t*)a.o);
+}
+
+template <int D>
+static hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
+  switch (a.block_size) {
+    case 16: launch_d_b<D, 16>(a, s); break;
+    case 32: launch_d_b<D, 32>(a, s); break;
+    case 64: launch_d_b<D, 64>(a, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
-  dim3 grid(a.n_tiles * a.n_kv_heads);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_bf16_kernel<128, kNW>), grid, dim3(kNW * 64), 0, s, a);
-  else if (a.head_dim == 64)
-    hipLaunchKernelGGL((attn_bf16_kernel<64, kNW>), grid, dim3(kNW * 64), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (a.head_dim == 128) return launch_d<128>(a, s);
+  if (a.head_dim == 64) return launch_d<64>(a, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace pgsr
