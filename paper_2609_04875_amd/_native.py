@@ -10,7 +10,9 @@ import ctypes
 import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "lib", "libpgsr.so")
+# PGSR_LIB may name another build of the same library (e.g. a variant built
+# with different compile-time options); the default is the in-tree build.
+LIB_PATH = os.environ.get("PGSR_LIB") or os.path.join(_PKG, "lib", "libpgsr.so")
 
 OK, EINVAL, ERANGE, ENOMEM, EUNSUPPORTED, EHIP = range(6)
 F32, BF16 = 0, 1

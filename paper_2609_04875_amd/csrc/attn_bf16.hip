@@ -8,21 +8,28 @@
 // same XCD (workgroups are dealt to the 8 XCDs round-robin) and share that
 // XCD's L2 copy of the head's keys and values.  Tiles are issued costliest
 // first (sequences sorted by work on the host, tiles within a sequence from
-// the last, longest-context one down).
+// the last, longest-context one down).  Two workgroups share a CU.
 //
 // Per key tile (KT = 64 keys at absolute positions kb .. kb+63):
 //   * K and V^T are gathered through the block table from HBM into registers
-//     one tile ahead, then stored to a double-buffered LDS tile (one barrier
-//     per tile).  Keys at or beyond the sequence length are zero-filled, never
-//     loaded.
+//     one tile ahead (block ids two tiles ahead), then stored to a
+//     double-buffered LDS tile: one barrier per tile.  Every load is
+//     unconditional (block index clamped to the sequence's last block); V
+//     entries of keys at or past the sequence length are zeroed before the
+//     LDS store, and such keys are masked out of S, so stale or NaN slots never
+//     reach the result.
 //   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = Q^T
 //     held in registers for the whole kernel).  In the 32x32 accumulator a lane
 //     holds one query column and 16 keys, so the row max and row sum are
 //     in-lane reductions plus one exchange between the two 32-lane halves.
+//     Operand reads are issued several MFMAs ahead of use.
 //   * Online softmax in the base-2 domain (log2(e) folded into the scale);
-//     the causal mask is a select to -inf on diagonal tiles only.  The O
-//     rescale is skipped when no row's maximum moved (alpha == 1 exactly, so
-//     the result is bitwise the same as always rescaling).
+//     the causal mask is a select to -inf on diagonal tiles only.  A row keeps
+//     its running maximum until a tile exceeds it by more than 2^8 (weights
+//     then stay below 256, harmless in fp32 / bf16), so the O rescale is rare;
+//     when any row of the wave needs it the wave rescales (alpha = 1 exactly
+//     for the others).  The row sum adds the bf16-rounded P values that enter
+//     the PV product (v_dot2_f32_bf16 against ones).
 //   * O^T += V^T P^T with the same MFMA (A = V^T rows from LDS, B = P^T taken
 //     straight from the S^T registers after rounding to bf16).  The reduction
 //     index of a B operand must match the A operand's, and a lane's S^T
@@ -30,9 +37,13 @@
 //     lane half); V^T is therefore stored in LDS with the 4-key chunks of every
 //     16-key group in the order [0, 2, 1, 3], which makes those 8 keys one
 //     contiguous 16-byte LDS read.
+// LDS rows are padded by 16 bytes (K: D+8 elements, V^T: 72), which spreads
+// the 32 rows one MFMA operand read touches over distinct bank groups and keeps
+// every operand address a base plus an immediate offset.
+//
 // Key tiles sit at absolute positions and rows never interact, so a query's
-// output bits depend only on its absolute position: selective replay and full
-// reset agree bitwise, and repeated runs are bitwise identical.
+// output bits depend only on its absolute position and its own keys: selective
+// replay and full reset agree bitwise, and repeated runs are bitwise identical.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -45,14 +56,19 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kNW = 4;   // waves per workgroup
-constexpr int kKT = 64;  // keys per tile
+constexpr int kNW = 4;      // waves per workgroup
+constexpr int kKT = 64;     // keys per tile
+constexpr int kAhead = 3;   // LDS operand reads issued this many MFMAs ahead
+constexpr float kSlack = 8.f;   // lazy rescale threshold, log2 units
+
+__device__ constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 
 // Value of the lane 32 apart (same query row, other half of the wave):
 // v_permlane32_swap exchanges the upper half of its first operand with the
@@ -66,7 +82,7 @@ __device__ inline float xor32(float x) {
 
 // Zero 16-bit elements e (0..7) of a 16-byte chunk for which pos0 + e >= limit.
 __device__ inline u32x4 zero_tail(u32x4 v, int pos0, int limit) {
-  const int keep = limit - pos0;  // elements to keep, < 8 here
+  const int keep = limit - pos0;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     const int e0 = 2 * w;
@@ -78,8 +94,15 @@ __device__ inline u32x4 zero_tail(u32x4 v, int pos0, int limit) {
   return v;
 }
 
+// Block ids of one key tile (up to four blocks), indexed with a wave-uniform
+// value through selects rather than as an array, which would live in memory.
+struct Ids {
+  int32_t v0, v1, v2, v3;
+  __device__ int32_t get(int i) const { return i == 0 ? v0 : i == 1 ? v1 : i == 2 ? v2 : v3; }
+};
+
 template <int D, int NW, int B>
-__global__ void __launch_bounds__(NW * 64, (NW == 4 ? 2 : 1))
+__global__ void __launch_bounds__(NW * 64, 2)
 attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t* __restrict__ qg_,
                  const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
                  uint16_t* __restrict__ og) {
@@ -91,6 +114,7 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   constexpr int CHB = B * D / 8;           // 16-byte chunks per block-head (K or V)
   constexpr int CPT = KT * D / 8 / NT;     // chunks per thread per tile (K or V)
   static_assert(CPT * NT * 8 == KT * D, "tile split");
+  static_assert(KB >= 1 && KB <= 4, "block size 16, 32 or 64");
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][KT * KLD];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][D * VLD];
 
@@ -147,32 +171,27 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
     else return tid % CHB;
   };
 
-  // Block ids of a key tile, clamped in range so every tile load is
-  // unconditional (out-of-range keys are masked later).  They are fetched two
-  // tiles ahead as a per-lane vector load (lane bi holds block bi's id; the
-  // vector-memory counter is in order, so waiting for a tile's data never waits
-  // on this), then broadcast to scalar registers with readlane.
-  int32_t ids[KB] = {}, idv = 0;
-  auto fetch_ids = [&](int kb) {
-    idv = row[min(kb / B + (lane < KB ? lane : 0), last_blk)];
-  };
+  // Block ids of a key tile, clamped in range.  They are fetched as a
+  // per-lane vector load (lane bi holds block bi's id) one tile before use,
+  // issued ahead of that tile's data loads so waiting for the data implies
+  // they have arrived, then broadcast to scalar registers with readlane.
+  int idv = 0;
+  auto fetch_ids = [&](int kt) { idv = row[min(kt * KB + (lane < KB ? lane : 0), last_blk)]; };
   auto take_ids = [&]() {
-#pragma unroll
-    for (int bi = 0; bi < KB; ++bi) ids[bi] = __builtin_amdgcn_readlane(idv, bi);
-  };
-  auto block_id = [&](int blk) {
-    int32_t id = ids[0];
-#pragma unroll
-    for (int bi = 1; bi < KB; ++bi) id = blk == bi ? ids[bi] : id;
-    return id;
+    Ids ids;
+    ids.v0 = __builtin_amdgcn_readlane(idv, 0);
+    ids.v1 = KB > 1 ? __builtin_amdgcn_readlane(idv, 1) : 0;
+    ids.v2 = KB > 2 ? __builtin_amdgcn_readlane(idv, 2) : 0;
+    ids.v3 = KB > 3 ? __builtin_amdgcn_readlane(idv, 3) : 0;
+    return ids;
   };
 
   u32x4 kreg[CPT], vreg[CPT];
-  auto load_tile = [&]() {
+  auto load_tile = [&](const Ids& ids) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int blk = chunk_blk(i), in = chunk_in(i);
-      const int64_t base = (head_base + (int64_t)block_id(blk) * hkv) * (B * D);
+      const int in = chunk_in(i);
+      const int64_t base = (head_base + (int64_t)ids.get(chunk_blk(i)) * hkv) * (B * D);
       kreg[i] = *(const u32x4*)(kc + base + (in / (D / 8)) * D + (in % (D / 8)) * 8);
       vreg[i] = *(const u32x4*)(vc + base + (in / (B / 8)) * B + (in % (B / 8)) * 8);
     }
@@ -203,31 +222,78 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   float m = -INFINITY, l = 0.f;
   const float c2 = a.scale_log2;
 
-  fetch_ids(0);
-  take_ids();
-  load_tile();
-  if (n_kt > 1) fetch_ids(KT);
+  // S^T = K Q^T for one 64-key tile: two independent 32-key accumulators.
+  auto qk = [&](int buf, f32x16 (&s)[2]) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
+    const uint16_t* kp = &k_lds[buf][r * KLD + 8 * hh];
+    constexpr int N = D / 16;
+    bf16x8 k0[N], k1[N];
+#pragma unroll
+    for (int ds = 0; ds < N; ++ds) {
+      k0[ds] = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 16 * ds));
+      k1[ds] = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 32 * KLD + 16 * ds));
+    }
+#pragma unroll
+    for (int ds = 0; ds < N; ++ds) {
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0[ds], qb[ds], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1[ds], qb[ds], s[1], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kAhead, 1);   // DS reads
+#pragma unroll
+    for (int ds = 0; ds < N; ++ds) {
+      if (ds + kAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);          // MFMAs
+    }
+  };
+  // O^T += V^T P^T for one tile: 16 keys per step.
+  auto pv = [&](int buf, const bf16x8 (&pb)[KT / 16]) {
+    constexpr int N = KT / 16 * (D / 32);
+    bf16x8 va[N];
+#pragma unroll
+    for (int ks = 0; ks < KT / 16; ++ks)
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+        va[ks * (D / 32) + db] = __builtin_bit_cast(
+            bf16x8, *(const u32x4*)&v_lds[buf][(db * 32 + r) * VLD + ks * 16 + 8 * hh]);
+#pragma unroll
+    for (int ks = 0; ks < KT / 16; ++ks)
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks * (D / 32) + db], pb[ks],
+                                                           oacc[db], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 2);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if (i + kAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+    }
+  };
+
+  // Prologue: tile 0 in registers, ids of tile 1 taken, tile 2's in flight.
+  Ids ids_n{};
+  {
+    fetch_ids(0);
+    const Ids ids0 = take_ids();
+    if (n_kt > 1) fetch_ids(1);
+    load_tile(ids0);
+    if (n_kt > 1) ids_n = take_ids();
+    if (n_kt > 2) fetch_ids(2);
+  }
+  // One step per key tile.  LDS buffer kt&1 receives tile kt before the
+  // barrier; it was last read at step kt-2, one barrier earlier.
   for (int kt = 0; kt < n_kt; ++kt) {
-    const int buf = kt & 1;
-    const int kb = kt * KT;
+    const int kb = kt * KT, buf = kt & 1;
     store_tile(buf, kb);
     __syncthreads();
     if (kt + 1 < n_kt) {
-      take_ids();                                  // fetched one tile ago
-      load_tile();                                 // tile kt+1
-      if (kt + 2 < n_kt) fetch_ids(kb + 2 * KT);
+      const Ids ids = ids_n;                       // tile kt+1
+      if (kt + 2 < n_kt) ids_n = take_ids();       // tile kt+2, fetched a step ago
+      if (kt + 3 < n_kt) fetch_ids(kt + 3);
+      load_tile(ids);
     }
-
-    // S^T = K Q^T for keys kb .. kb+63: two independent 32-key accumulators.
-    f32x16 s[2] = {f32x16{}, f32x16{}};
-    const uint16_t* kp = &k_lds[buf][r * KLD + 8 * hh];
-#pragma unroll
-    for (int ds = 0; ds < D / 16; ++ds) {
-      const bf16x8 k0 = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 16 * ds));
-      const bf16x8 k1 = __builtin_bit_cast(bf16x8, *(const u32x4*)(kp + 32 * KLD + 16 * ds));
-      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[ds], s[0], 0, 0, 0);
-      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[ds], s[1], 0, 0, 0);
-    }
+    f32x16 s[2];
+    qk(buf, s);
     // Causal mask (select) where some key may lie past some row's position.
     if (kb + KT - 1 > first_q) {
 #pragma unroll
@@ -243,39 +309,34 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
     for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kh][i]);
-    mx = fmaxf(mx, xor32(mx));
-    const float m_new = fmaxf(m, mx * c2);
+    mx = fmaxf(mx, xor32(mx)) * c2;                // tile max of the row, log2 units
+    const bool bump = mx > m + kSlack;             // first tile: m = -inf
+    const float m_new = bump ? mx : m;
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m - m_use);
-    float psum = 0.f;
-#pragma unroll
-    for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kh][i], c2, -m_use));
-        s[kh][i] = p;
-        psum += p;
-      }
-    l = fmaf(l, alpha, psum);
+    const float alpha = bump ? __builtin_amdgcn_exp2f(m - m_use) : 1.f;
     m = m_new;
-    if (__ballot(alpha != 1.f)) {
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
-    }
-    // O^T += V^T P^T, 16 keys per step.
+    // P = exp2(s*c - m) rounded to bf16; the row sum adds exactly those values.
+    bf16x8 pb[KT / 16];
+    float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KT / 16; ++ks) {
       const int kh = ks >> 1, o8 = (ks & 1) * 8;
-      f32x8 pv = {s[kh][o8 + 0], s[kh][o8 + 1], s[kh][o8 + 2], s[kh][o8 + 3],
-                  s[kh][o8 + 4], s[kh][o8 + 5], s[kh][o8 + 6], s[kh][o8 + 7]};
-      const bf16x8 pb = __builtin_convertvector(pv, bf16x8);
-      const uint16_t* vp = &v_lds[buf][r * VLD + ks * 16 + 8 * hh];
+      f32x8 pv8;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        bf16x8 va = __builtin_bit_cast(bf16x8, *(const u32x4*)(vp + db * 32 * VLD));
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, oacc[db], 0, 0, 0);
-      }
+      for (int j = 0; j < 8; ++j) pv8[j] = __builtin_amdgcn_exp2f(fmaf(s[kh][o8 + j], c2, -m_use));
+      pb[ks] = __builtin_convertvector(pv8, bf16x8);
+      const bf16x2* p2 = (const bf16x2*)&pb[ks];
+      ps0 = __builtin_amdgcn_fdot2_f32_bf16(p2[0], kOnes, ps0, false);
+      ps1 = __builtin_amdgcn_fdot2_f32_bf16(p2[1], kOnes, ps1, false);
+      ps0 = __builtin_amdgcn_fdot2_f32_bf16(p2[2], kOnes, ps0, false);
+      ps1 = __builtin_amdgcn_fdot2_f32_bf16(p2[3], kOnes, ps1, false);
     }
+    l = fmaf(l, alpha, ps0 + ps1);
+    if (__ballot(bump)) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
+    }
+    pv(buf, pb);
   }
 
   const float l_tot = l + xor32(l);
