@@ -1,19 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of the selective-replay hot path on one MI355X.
 
-One step = restore by crop (Algorithm 1, restore step) + one replay prefill of
-the sanitized suffix (Algorithm 1, replay loop, prefill form), on the 8B
-attention geometry: 32 query / 8 KV heads, d = 128, bf16, a contaminated cache
-of 10240 tokens cropped to 8189 (unaligned to the 16-token block) and a
-2048-token suffix replayed against it.  Inputs are seeded synthetic tensors
-resident in HBM before timing starts.
+One step = restore by crop (Algorithm 1, restore step) + the replay prefill of
+the sanitized suffix (Algorithm 1, replay loop, prefill form).  The default
+workload is the 8B attention geometry: 32 query / 8 KV heads, d = 128, bf16, a
+contaminated cache of 10240 tokens cropped to 8189 (not a multiple of the
+16-token block) and a 2048-token suffix replayed against it.  ``--workload``
+selects the other workloads (tiny fp32 episode, 16 ragged episodes in one
+varlen launch, 32k-prefix chunked replay).  Inputs are seeded synthetic
+tensors resident in HBM before timing starts.
 
 A crop is destructive, so before every step the pre-crop block table, lengths
 and free list (a few KB) are copied back outside the timed region; each step
 is then bracketed by synchronisations and timed with HIP events on the stream
 the library launches on.  The library's own event hook times the attention
-kernel inside every timed step (the roofline figure).  The CPU baseline runs
-the fp64 oracle on a bounded sample of the same workload's query rows.
+kernel (the roofline figure): inside every timed step when a step is a single
+replay call, else in a separate pass.  The CPU baseline runs the fp64 oracle on
+a bounded sample of the same workload's query rows.
 
 Prints one JSON line.
 """
@@ -31,8 +34,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "suffix replay prefill tokens/s + attention TFLOP/s (% of bf16 MFMA peak)"
-PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA, published
-PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense bf16 MFMA; fp32 vector
+DEFAULT = "llama8b_p8189_s2048_bf16"
 
 
 def attention_flops(P: int, S: int, hq: int, d: int) -> float:
@@ -40,38 +43,159 @@ def attention_flops(P: int, S: int, hq: int, d: int) -> float:
     return 4.0 * hq * d * (S * P + S * (S + 1) / 2.0)
 
 
-def to_dev(arr, torch):
-    return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).cuda()
+def attention_bytes(P: int, S: int, hq: int, hkv: int, d: int, eb: int) -> float:
+    """Algorithmic HBM bytes of one attention launch: Q and O, K/V of 0..P+S-1."""
+    return eb * (2.0 * S * hq * d + 2.0 * (P + S) * hkv * d)
 
 
-def cpu_baseline(ep, w, budget_s: float):
+class Setup:
+    """Device-resident episodes, a pool holding their contaminated runs, and
+    the replay inputs; ``step()`` runs one crop + replay."""
+
+    def __init__(self, name: str):
+        import torch
+        import workloads as W
+        from paper_2609_04875_amd import BF16, F32, KVPool
+
+        self.torch = torch
+        self.w = w = W.workload(name)
+        g = w.geometry
+        if name.startswith("ragged"):
+            self.eps = W.ragged_episodes(w)
+        else:
+            self.eps = [W.single_episode(w)]
+        self.chunk = w.chunk or None
+        B = w.block_size
+        nb = sum(-(-e.t_contaminated // B) + -(-e.t_sanitized // B) for e in self.eps) + 8
+        max_bps = max(-(-max(e.t_contaminated, e.t_sanitized) // B) for e in self.eps) + 4
+        self.pool = KVPool(1, g.n_q_heads, g.n_kv_heads, g.head_dim, nb, len(self.eps), max_bps,
+                           F32 if w.dtype == "f32" else BF16, B)
+        dev = lambda a: self._dev(a)
+        for i, ep in enumerate(self.eps):
+            cq, ck, cv = (dev(ep.contaminated(x)) for x in ("q", "k", "v"))
+            assert self.pool.replay(0, [i], [ep.t_contaminated], cq, ck, cv, torch.empty_like(cq),
+                                    w.scale) == 0
+            del cq, ck, cv
+        torch.cuda.synchronize()
+        self.saved = self.pool.save_meta()
+        self.seqs = list(range(len(self.eps)))
+        self.q = torch.cat([dev(e.q[e.prefix:]) for e in self.eps])
+        self.k = torch.cat([dev(e.k[e.prefix:]) for e in self.eps])
+        self.v = torch.cat([dev(e.v[e.prefix:]) for e in self.eps])
+        self.o = torch.empty_like(self.q)
+        self.S = [e.suffix for e in self.eps]
+        self.P = [e.prefix for e in self.eps]
+
+    def _dev(self, a):
+        torch = self.torch
+        if self.w.dtype == "f32":
+            return torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    @property
+    def calls_per_step(self) -> int:
+        return -(-self.S[0] // self.chunk) if self.chunk else 1
+
+    def restore(self) -> None:
+        self.pool.load_meta(self.saved)
+
+    def step(self, ev=None) -> None:
+        """crop + replay; optional events: ev[0] start, ev[1] after crop, ev[2] end."""
+        torch = self.torch
+        s = torch.cuda.current_stream()
+        if ev:
+            ev[0].record(s)
+        if self.pool.crop(self.seqs, self.P):
+            raise RuntimeError("crop failed")
+        if ev:
+            ev[1].record(s)
+        if self.chunk:
+            for c0 in range(0, self.S[0], self.chunk):
+                sl = slice(c0, c0 + self.chunk)
+                if self.pool.replay(0, [0], [self.chunk], self.q[sl], self.k[sl], self.v[sl],
+                                    self.o[sl], self.w.scale):
+                    raise RuntimeError("replay failed")
+        elif self.pool.replay(0, self.seqs, self.S, self.q, self.k, self.v, self.o, self.w.scale):
+            raise RuntimeError("replay failed")
+        if ev:
+            ev[2].record(s)
+
+    def flops(self) -> float:
+        g = self.w.geometry
+        return sum(attention_flops(p, s, g.n_q_heads, g.head_dim) for p, s in zip(self.P, self.S))
+
+    def bytes(self) -> float:
+        g = self.w.geometry
+        eb = 4 if self.w.dtype == "f32" else 2
+        if self.chunk:  # each chunk re-reads the prefix grown so far
+            P, S, C = self.P[0], self.S[0], self.chunk
+            return sum(attention_bytes(P + c0, C, g.n_q_heads, g.n_kv_heads, g.head_dim, eb)
+                       for c0 in range(0, S, C))
+        return sum(attention_bytes(p, s, g.n_q_heads, g.n_kv_heads, g.head_dim, eb)
+                   for p, s in zip(self.P, self.S))
+
+
+def cpu_baseline(st: Setup, budget_s: float):
     """fp64 oracle on a bounded, evenly spaced sample of suffix tokens (all heads)."""
     import oracle
     import workloads as W
 
-    P, S = ep.prefix, ep.suffix
-    hq, d = w.geometry.n_q_heads, w.geometry.head_dim
-    f64 = lambda a: W.bf16_bits_to_f32(a).astype(np.float64)
-    q, k, v = f64(ep.q[P:]), f64(ep.k), f64(ep.v)
+    w = st.w
+    hq = w.geometry.n_q_heads
+    f64 = (lambda a: a.astype(np.float64)) if w.dtype == "f32" else \
+        (lambda a: W.bf16_bits_to_f32(a).astype(np.float64))
+    prepared = [(e, f64(e.q[e.prefix:]), f64(e.k), f64(e.v)) for e in st.eps]
+    total_tokens = sum(st.S)
 
-    def run(n_tok):
-        toks = np.linspace(0, S - 1, n_tok).round().astype(np.int64)
-        rows = (toks[:, None] * hq + np.arange(hq)[None, :]).reshape(-1)
-        pool = oracle.PoolModel(2 * (ep.t_contaminated // w.block_size + 2), 1,
-                                ep.t_contaminated // w.block_size + 2, w.block_size)
-        pool.reserve([0], [ep.t_contaminated]); pool.commit([0], [ep.t_contaminated])
+    def run(frac):
         t0 = time.perf_counter()
-        pool.crop([0], [P])
-        pool.reserve([0], [S]); pool.commit([0], [S])
-        oracle.attention(q, k, v, P, w.scale, rows=rows)
-        return time.perf_counter() - t0
+        n_done = 0
+        for e, q, k, v in prepared:
+            n_tok = max(1, int(round(frac * e.suffix)))
+            toks = np.linspace(0, e.suffix - 1, n_tok).round().astype(np.int64)
+            rows = (toks[:, None] * hq + np.arange(hq)[None, :]).reshape(-1)
+            pool = oracle.PoolModel(2 * (e.t_contaminated // w.block_size + 2), 1,
+                                    e.t_contaminated // w.block_size + 2, w.block_size)
+            pool.reserve([0], [e.t_contaminated]); pool.commit([0], [e.t_contaminated])
+            pool.crop([0], [e.prefix])
+            pool.reserve([0], [e.suffix]); pool.commit([0], [e.suffix])
+            oracle.attention(q, k, v, e.prefix, w.scale, rows=rows)
+            n_done += n_tok
+        return n_done, time.perf_counter() - t0
 
-    dt = run(4)
-    n_tok = int(max(4, min(S, 4 * budget_s / max(dt, 1e-6))))
-    dt = run(n_tok)
-    return {"value": n_tok / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
-            "sample": f"{n_tok} of {S} suffix tokens (evenly spaced, all {hq} heads), "
-                      f"fp64, {dt:.1f} s incl. crop + reserve on the oracle pool"}
+    n, dt = run(min(1.0, 64.0 / total_tokens))
+    frac = min(1.0, (n / total_tokens) * budget_s / max(dt, 1e-6))
+    n, dt = run(frac)
+    return {"value": n / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{n} of {total_tokens} suffix tokens (evenly spaced in each episode, all "
+                      f"{hq} heads), fp64, {dt:.1f} s incl. crop + reserve on the oracle pool"}
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per attention launch from the committed counter summary
+    (FETCH_SIZE, WRITE_SIZE scaled by a plain copy of known size), or None when
+    there is none for this workload or the kernel source changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attn_bf16_{workload.replace('_bf16', '')}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    with open(os.path.join(ROOT, rec["kernel_source"]), "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != rec["kernel_source_sha256"]:
+            return None
+    return rec["traffic_bytes_per_dispatch"]
+
+
+def copy_calibration(mib: int) -> None:
+    """A plain device copy of known size, for scaling FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
 
 
 def main() -> int:
@@ -79,8 +203,11 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="after timing, copy this many MiB device-to-device (counter scaling)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -90,51 +217,52 @@ def main() -> int:
 
     import torch
 
-    import workloads as W
-    from paper_2609_04875_amd import BF16, KVPool
-
-    w = W.workload("llama8b_p8189_s2048_bf16")
-    g = w.geometry
-    ep = W.single_episode(w)
-    P, S, Tc = ep.prefix, ep.suffix, ep.t_contaminated
     torch.cuda.set_device(0)
-    stream = torch.cuda.current_stream()
-    nb = -(-Tc // w.block_size) + -(-(P + S) // w.block_size) + 8
-    pool = KVPool(1, g.n_q_heads, g.n_kv_heads, g.head_dim, nb, 1, -(-Tc // w.block_size) + 4, BF16,
-                  w.block_size)
-    cq, ck, cv = (to_dev(ep.contaminated(x), torch) for x in ("q", "k", "v"))
-    assert pool.replay(0, [0], [Tc], cq, ck, cv, torch.empty_like(cq), w.scale) == 0
-    torch.cuda.synchronize()
-    contaminated = pool.save_meta()
-    q, k, v = (to_dev(getattr(ep, x)[P:], torch) for x in ("q", "k", "v"))
-    o = torch.empty_like(q)
-    del cq, ck, cv
-    pool.enable_timing(True)
-
+    st = Setup(args.workload)
+    w, g, pool = st.w, st.w.geometry, st.pool
+    single_call = st.calls_per_step == 1
+    pool.enable_timing(single_call)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     step_ms, crop_ms, attn_ms, append_ms = [], [], [], []
     for i in range(args.warmup + args.steps):
-        pool.load_meta(contaminated)          # outside the timed region
+        st.restore()                          # outside the timed region
         torch.cuda.synchronize()
-        ev[0].record(stream)
-        rc1 = pool.crop([0], [P])
-        ev[1].record(stream)
-        rc2 = pool.replay(0, [0], [S], q, k, v, o, w.scale)
-        ev[2].record(stream)
+        st.step(ev)
         torch.cuda.synchronize()
-        if rc1 or rc2:
-            raise RuntimeError(f"crop/replay failed: {rc1} {rc2}")
         if i >= args.warmup:
             step_ms.append(ev[0].elapsed_time(ev[2]))
             crop_ms.append(ev[0].elapsed_time(ev[1]))
-            a_ms, t_ms = pool.last_times()
-            append_ms.append(a_ms)
-            attn_ms.append(t_ms)
+            if single_call:
+                a_ms, t_ms = pool.last_times()
+                append_ms.append(a_ms)
+                attn_ms.append(t_ms)
+    if not single_call:
+        # kernel times per replay call, in a pass of its own (each call waits
+        # for its events, which would stretch the timed steps)
+        pool.enable_timing(True)
+        for _ in range(3):
+            st.restore()
+            torch.cuda.synchronize()
+            pool.crop(st.seqs, st.P)
+            a_tot = t_tot = 0.0
+            for c0 in range(0, st.S[0], st.chunk):
+                sl = slice(c0, c0 + st.chunk)
+                pool.replay(0, [0], [st.chunk], st.q[sl], st.k[sl], st.v[sl], st.o[sl], w.scale)
+                a_ms, t_ms = pool.last_times()
+                a_tot += a_ms
+                t_tot += t_ms
+            append_ms.append(a_tot)
+            attn_ms.append(t_tot)
+        pool.enable_timing(False)
+    if args.calibrate_copy_mib:
+        copy_calibration(args.calibrate_copy_mib)
+
     total_s = sum(step_ms) / 1e3
-    tokens = S * args.steps
-    flops = attention_flops(P, S, g.n_q_heads, g.head_dim)
+    tokens = sum(st.S) * args.steps
+    flops, nbytes = st.flops(), st.bytes()
     attn_mean = float(np.mean(attn_ms))
     achieved = flops / (attn_mean * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
     result = {
         "metric": METRIC,
         "value": tokens / total_s,
@@ -146,21 +274,27 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "prefix": P, "suffix": S, "contaminated": Tc,
-                   "n_q_heads": g.n_q_heads, "n_kv_heads": g.n_kv_heads, "head_dim": g.head_dim,
-                   "block_size": w.block_size, "episodes": 1, "recomputed_tokens": S},
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                     "kernel": "attn_bf16_kernel<128,4>", "flops_per_launch": flops,
-                     "kernel_ms": attn_mean},
+        "config": {"workload": w.name, "episodes": len(st.eps), "prefix": st.P if len(st.P) > 1 else st.P[0],
+                   "suffix": st.S if len(st.S) > 1 else st.S[0],
+                   "contaminated": [e.t_contaminated for e in st.eps] if len(st.eps) > 1 else st.eps[0].t_contaminated,
+                   "chunk": st.chunk, "n_q_heads": g.n_q_heads, "n_kv_heads": g.n_kv_heads,
+                   "head_dim": g.head_dim, "block_size": w.block_size,
+                   "recomputed_tokens": sum(st.S)},
+        "roofline": {"bound": "mfma" if w.dtype == "bf16" else "alu", "achieved": achieved,
+                     "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "kernel": ("attn_bf16_kernel<128,4,16>" if w.dtype == "bf16"
+                                else f"attn_f32_kernel<{g.head_dim}>"),
+                     "flops_per_step": flops, "algorithmic_bytes_per_step": nbytes,
+                     "kernel_ms": attn_mean, "kernel_launches_per_step": st.calls_per_step,
+                     "algorithmic_GBps": nbytes / (attn_mean * 1e-3) / 1e9},
         "breakdown_ms": {"crop": float(np.mean(crop_ms)), "append": float(np.mean(append_ms)),
                          "attention": attn_mean, "step": total_s * 1e3 / args.steps,
                          "step_min": float(np.min(step_ms))},
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(ep, w, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(st, args.cpu_seconds)
     print(json.dumps(result), flush=True)
     return 0
 
