@@ -55,7 +55,7 @@ class Setup:
     def __init__(self, name: str):
         import torch
         import workloads as W
-        from paper_2609_04875_amd import BF16, F32, KVPool
+        from paper_2609_04875_amd import BF16, F32, KVPool, workspace_bytes
 
         self.torch = torch
         self.w = w = W.workload(name)
@@ -68,8 +68,11 @@ class Setup:
         B = w.block_size
         nb = sum(-(-e.t_contaminated // B) + -(-e.t_sanitized // B) for e in self.eps) + 8
         max_bps = max(-(-max(e.t_contaminated, e.t_sanitized) // B) for e in self.eps) + 4
+        # workspace for split-key launches (partial softmax states) where a
+        # replay call is too small to fill the GPU: the chunked workload
+        ws = workspace_bytes(g.n_q_heads, g.head_dim, self.chunk) if self.chunk else 0
         self.pool = KVPool(1, g.n_q_heads, g.n_kv_heads, g.head_dim, nb, len(self.eps), max_bps,
-                           F32 if w.dtype == "f32" else BF16, B)
+                           F32 if w.dtype == "f32" else BF16, B, workspace_bytes=ws)
         dev = lambda a: self._dev(a)
         for i, ep in enumerate(self.eps):
             cq, ck, cv = (dev(ep.contaminated(x)) for x in ("q", "k", "v"))

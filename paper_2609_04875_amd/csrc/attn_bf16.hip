@@ -60,6 +60,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -120,7 +121,8 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
 
   const int hkv = a.n_kv_heads;
   const int g = blockIdx.x % hkv;
-  const int tile = blockIdx.x / hkv;
+  const int split = (blockIdx.x / hkv) % a.n_splits;
+  const int tile = blockIdx.x / hkv / a.n_splits;
   int ei = 0;
   while (ei + 1 < a.n && a.e[ei + 1].tile_start <= tile) ++ei;
   const AttnEntry e = a.e[ei];
@@ -138,9 +140,14 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   const int qpos = valid ? e.prefix + tok : -1;
   const int t_last = min(e.q_len, t0 + TW) - 1;
   const int kv_len = e.prefix + e.q_len;
-  const int key_end = e.prefix + t_last + 1;
-  const int n_kt = (key_end + KT - 1) / KT;
   const int first_q = e.prefix + t0;               // smallest query position here
+  // Keys this workgroup visits: [key_lo, key_end), whole tiles at absolute
+  // positions (a split boundary is a multiple of the tile size).
+  const int key_lo = split * a.split_len;
+  const int key_end = min(e.prefix + t_last + 1, a.n_splits > 1 ? key_lo + a.split_len : INT32_MAX);
+  if (key_lo >= key_end) return;                   // nothing of this tile in this split
+  const int kt0 = key_lo / KT;
+  const int n_kt = (key_end + KT - 1) / KT;
 
   // Q^T operand: lane holds Q[row][16*ds + 8*hh .. +7] for each ds.
   bf16x8 qb[D / 16];
@@ -270,19 +277,20 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
     }
   };
 
-  // Prologue: tile 0 in registers, ids of tile 1 taken, tile 2's in flight.
+  // Prologue: tile kt0 in registers, ids of the next taken, the one after in
+  // flight.
   Ids ids_n{};
   {
-    fetch_ids(0);
+    fetch_ids(kt0);
     const Ids ids0 = take_ids();
-    if (n_kt > 1) fetch_ids(1);
+    if (kt0 + 1 < n_kt) fetch_ids(kt0 + 1);
     load_tile(ids0);
-    if (n_kt > 1) ids_n = take_ids();
-    if (n_kt > 2) fetch_ids(2);
+    if (kt0 + 1 < n_kt) ids_n = take_ids();
+    if (kt0 + 2 < n_kt) fetch_ids(kt0 + 2);
   }
   // One step per key tile.  LDS buffer kt&1 receives tile kt before the
-  // barrier; it was last read at step kt-2, one barrier earlier.
-  for (int kt = 0; kt < n_kt; ++kt) {
+  // barrier; it was last read two steps earlier, one barrier before.
+  for (int kt = kt0; kt < n_kt; ++kt) {
     const int kb = kt * KT, buf = kt & 1;
     store_tile(buf, kb);
     __syncthreads();
@@ -340,7 +348,18 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   }
 
   const float l_tot = l + xor32(l);
-  if (valid) {
+  if (valid && a.n_splits > 1) {                   // unnormalised partials, fp32
+    const int64_t prow = (int64_t)split * a.n_rows + (int64_t)(e.q_off + tok) * a.n_q_heads + hq;
+    float* acc = a.ws_acc + prow * D + 4 * hh;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4)
+        *(f32x4*)(acc + db * 32 + 8 * i4) =
+            f32x4{oacc[db][4 * i4 + 0], oacc[db][4 * i4 + 1], oacc[db][4 * i4 + 2],
+                  oacc[db][4 * i4 + 3]};
+    if (hh == 0) *(f32x2*)(a.ws_ml + 2 * prow) = f32x2{m, l_tot};
+  } else if (valid) {
     const float inv = 1.f / l_tot;
     uint16_t* op = og + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 4 * hh;
 #pragma unroll
@@ -354,13 +373,53 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   }
 }
 
+// Split-key combine: for query row r with position p, the splits s with
+// s * split_len <= p hold partials (m_s, l_s, acc_s); splits starting past p
+// saw no visible key and may hold stale data, so they are skipped.
+//   M = max m_s,  w_s = 2^(m_s - M),  o = sum_s w_s acc_s / sum_s w_s l_s,
+// summed in increasing s.  16 threads per row, 8 columns each.
+template <int D>
+__global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t* __restrict__ og) {
+  constexpr int TPR = D / 8;                       // threads per row
+  const int64_t row = (int64_t)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+  const int c0 = (threadIdx.x % TPR) * 8;
+  if (row >= a.n_rows) return;
+  const int tok = (int)(row / a.n_q_heads);        // packed query token
+  int ei = 0;                                      // entries are not sorted by q_off
+  for (int i = 0; i < a.n; ++i)
+    if (tok >= a.e[i].q_off && tok < a.e[i].q_off + a.e[i].q_len) ei = i;
+  const AttnEntry e = a.e[ei];
+  const int qpos = e.prefix + (tok - e.q_off);
+  const int ns = min(a.n_splits, qpos / a.split_len + 1);
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ws_ml[2 * ((int64_t)s * a.n_rows + row)]);
+  float L = 0.f;
+  f32x4 o0 = {0, 0, 0, 0}, o1 = {0, 0, 0, 0};
+  for (int s = 0; s < ns; ++s) {
+    const int64_t prow = (int64_t)s * a.n_rows + row;
+    const float wgt = __builtin_amdgcn_exp2f(a.ws_ml[2 * prow] - M);
+    L = fmaf(wgt, a.ws_ml[2 * prow + 1], L);
+    const f32x4* acc = (const f32x4*)(a.ws_acc + prow * D + c0);
+    o0 += wgt * acc[0];
+    o1 += wgt * acc[1];
+  }
+  const float inv = 1.f / L;
+  bf16x8 out;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    out[j] = (__bf16)(o0[j] * inv);
+    out[4 + j] = (__bf16)(o1[j] * inv);
+  }
+  *(bf16x8*)(og + row * D + c0) = out;
+}
+
 }  // namespace
 
 int attn_bf16_tile_tokens(int, int group) { return kNW * 32 / group; }
 
 template <int D, int B>
 static void launch_d_b(const AttnArgs& a, hipStream_t s) {
-  dim3 grid(a.n_tiles * a.n_kv_heads);
+  dim3 grid(a.n_tiles * a.n_kv_heads * a.n_splits);
   hipLaunchKernelGGL((attn_bf16_kernel<D, kNW, B>), grid, dim3(kNW * 64), 0, s, a, a.tables,
                      (const uint16_t*)a.q, (const uint16_t*)a.k_cache,
                      (const uint16_t*)a.v_cache, (uint16_t*)a.o);
@@ -374,6 +433,19 @@ static hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
     case 64: launch_d_b<D, 64>(a, s); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.n_rows <= 0) return hipSuccess;
+  const int rows_per_block = 256 / (a.head_dim / 8);
+  dim3 grid((a.n_rows + rows_per_block - 1) / rows_per_block);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL(split_combine_kernel<128>, grid, dim3(256), 0, s, a, (uint16_t*)a.o);
+  else if (a.head_dim == 64)
+    hipLaunchKernelGGL(split_combine_kernel<64>, grid, dim3(256), 0, s, a, (uint16_t*)a.o);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

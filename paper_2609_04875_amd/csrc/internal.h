@@ -96,6 +96,16 @@ struct AttnArgs {
   float scale_log2;    // softmax_scale * log2(e)
   int32_t n;
   int32_t n_tiles;
+  // Split-key mode (n_splits > 1): split s of a query tile covers keys
+  // [s * split_len, (s+1) * split_len) at absolute positions and writes
+  // unnormalised partials for every query row r (r = token * n_q_heads + head
+  // over the launch's packed queries): acc to ws_acc[(s * n_rows + r) * D],
+  // the running max (log2 units) and row sum to ws_ml[2 * (s * n_rows + r)].
+  int32_t n_splits;
+  int32_t split_len;
+  int32_t n_rows;
+  float* ws_acc;
+  float* ws_ml;
   AttnEntry e[kMaxSeqsPerLaunch];
 };
 
@@ -108,6 +118,8 @@ hipError_t launch_poison(const PoisonArgs& a, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
+// Merge split-key partials into O (bf16), splits in increasing order.
+hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
                             int32_t* free_list, int32_t n_blocks, int32_t* free_top,
                             hipStream_t s);

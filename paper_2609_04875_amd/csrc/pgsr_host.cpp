@@ -139,6 +139,13 @@ struct Seg {
   int32_t seq, prefix, q_len, q_off;
 };
 
+// Split-key attention: used when a launch has fewer workgroups than this (two
+// per CU of the 256) and a workspace is available; at most kMaxSplits splits,
+// split boundaries at multiples of the 64-key tile.
+constexpr int64_t kSplitTargetWorkgroups = 512;
+constexpr int64_t kMaxSplits = 16;
+constexpr int32_t kSplitAlign = 64;
+
 // Validation of a replay step: lengths, table width, free blocks.
 int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
                  const int32_t* q_lens, const void* q, const void* k, const void* v,
@@ -279,7 +286,28 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
       tiles += cdiv(chunk[i].q_len, tile_tokens);
     }
     a.n_tiles = tiles;
+    a.n_splits = 1;
+    a.split_len = 0;
+    a.n_rows = off * p->hq;                        // packed query rows of the whole call
+    // Split-key mode when the launch would leave CUs idle and the caller gave
+    // a workspace for the partials: splits at absolute multiples of split_len.
+    const int64_t wgs = (int64_t)tiles * p->hkv;
+    if (p->dtype == PGSR_BF16 && p->workspace && wgs < kSplitTargetWorkgroups) {
+      int32_t max_key = 0;
+      for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);
+      const int64_t per_split = (int64_t)a.n_rows * ((int64_t)p->d + 2) * (int64_t)sizeof(float);
+      int64_t ns = std::min<int64_t>(kMaxSplits, (kSplitTargetWorkgroups + wgs - 1) / wgs);
+      ns = std::min<int64_t>(ns, (int64_t)(p->workspace_bytes / std::max<int64_t>(per_split, 1)));
+      if (ns > 1) {
+        const int32_t len = cdiv(cdiv(max_key, ns), kSplitAlign) * kSplitAlign;
+        a.n_splits = cdiv(max_key, len);
+        a.split_len = len;
+        a.ws_acc = (float*)p->workspace;
+        a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
+      }
+    }
     hipError_t err = p->dtype == PGSR_F32 ? launch_attn_f32(a, st) : launch_attn_bf16(a, st);
+    if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine_bf16(a, st);
     if (err != hipSuccess) return hip_fail(err, "attention launch");
   }
 

@@ -136,6 +136,11 @@ class KVPool:
         self.refresh()
 
 
+def workspace_bytes(n_q_heads: int, head_dim: int, max_total_q: int, max_splits: int = 16) -> int:
+    """Workspace that lets replays of up to max_total_q query tokens split keys."""
+    return int(N.lib.pgsr_workspace_bytes(n_q_heads, head_dim, max_total_q, max_splits))
+
+
 def gemm_bf16(x: torch.Tensor, w: torch.Tensor, r: Optional[torch.Tensor] = None,
               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """Y = X W (+ R) on the library's MFMA GEMM; bf16 in and out, fp32 accumulation."""
