@@ -174,9 +174,11 @@ int pgsr_pool_last_times(pgsr_pool *pool, float *append_ms, float *attention_ms)
 
 /*
  * Dense projection of the stacked-layer transition F (theta in Eq. (1)):
- * Y[m][n] = X[m][k] . W[k][n] (+ R[m][n] when R != NULL), bf16 row-major
- * device arrays, fp32 accumulation, one round-to-nearest-even store.  R may
- * alias Y.  m, n, k >= 0; n and k must be multiples of 8.
+ * Y[m][n] = sum_k X[m][k] * W[n][k] (+ R[m][n] when R != NULL), i.e. Y = X W^T
+ * with W in the linear-layer layout [n][k]; bf16 row-major device arrays,
+ * fp32 accumulation, one round-to-nearest-even store.  R may alias Y.
+ * m, n, k >= 0; n and k must be multiples of 8.  Rows of Y are computed
+ * independently with a fixed accumulation order (no split over k).
  */
 int pgsr_gemm_bf16(int32_t m, int32_t n, int32_t k, const void *x, const void *w,
                    const void *r, void *y, void *stream);

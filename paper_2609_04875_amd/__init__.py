@@ -10,6 +10,7 @@ package only allocates device memory with torch and marshals arguments.
 from ._native import (BF16, COMMIT, EHIP, EINVAL, ENOMEM, EUNSUPPORTED, ERANGE, F32, OK, POISON,
                       PgsrError)
 from .pool import KVPool, gemm_bf16, workspace_bytes
+from .stack import StackedReplay
 
-__all__ = ["KVPool", "gemm_bf16", "workspace_bytes", "PgsrError", "OK", "EINVAL", "ERANGE", "ENOMEM",
+__all__ = ["KVPool", "StackedReplay", "gemm_bf16", "workspace_bytes", "PgsrError", "OK", "EINVAL", "ERANGE", "ENOMEM",
            "EUNSUPPORTED", "EHIP", "F32", "BF16", "COMMIT", "POISON"]

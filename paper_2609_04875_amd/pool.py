@@ -143,9 +143,10 @@ def workspace_bytes(n_q_heads: int, head_dim: int, max_total_q: int, max_splits:
 
 def gemm_bf16(x: torch.Tensor, w: torch.Tensor, r: Optional[torch.Tensor] = None,
               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Y = X W (+ R) on the library's MFMA GEMM; bf16 in and out, fp32 accumulation."""
+    """Y = X W^T (+ R) on the library's MFMA GEMM, W in the [n][k] layout;
+    bf16 in and out, fp32 accumulation."""
     m, k = x.shape
-    k2, n = w.shape
+    n, k2 = w.shape
     if k2 != k:
         raise ValueError("inner dimensions differ")
     if out is None:

@@ -1,0 +1,110 @@
+"""Stacked-layer transition F (a reading: the paper defines no layer) on the
+GPU: the MFMA GEMM against fp64, and crop + replay of a small stack against
+the oracle's stacked layers and against the GPU full reset (Theorem 1,
+bitwise: every step is row-independent with a fixed accumulation order)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from gpu_helpers import assert_close, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16_dev(a: np.ndarray) -> torch.Tensor:
+    bits = W.f32_to_bf16_bits(np.ascontiguousarray(a, np.float32))
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _f64(t: torch.Tensor) -> np.ndarray:
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("m,n,k,res", [(1, 8, 8, False), (37, 136, 72, True), (128, 128, 64, False),
+                                       (300, 1024, 520, True), (257, 264, 1024, False),
+                                       (1000, 1024, 8192, True)])
+def test_gemm_matches_fp64(m, n, k, res):
+    from paper_2609_04875_amd import gemm_bf16
+    rng = np.random.default_rng(m * 7 + n)
+    x = rng.standard_normal((m, k)).astype(np.float32)
+    w = (rng.standard_normal((n, k)) / np.sqrt(k)).astype(np.float32)     # [n][k]
+    r = rng.standard_normal((m, n)).astype(np.float32) if res else None
+    xd, wd = _bf16_dev(x), _bf16_dev(w)
+    rd = _bf16_dev(r) if res else None
+    y = gemm_bf16(xd, wd, r=rd)
+    ref = _f64(xd) @ _f64(wd).T + (_f64(rd) if res else 0.0)
+    want = oracle.bf16_round(ref)
+    got = _f64(y)
+    # One bf16 rounding of an fp32 sum vs of the exact sum: one bf16 ulp (taken
+    # at the larger magnitude: the two may straddle a power of 2) plus the fp32
+    # accumulation error, which is absolute in the size of the terms (it
+    # dominates where the sum cancels to near zero).
+    ulp = np.maximum(np.abs(want), np.abs(got)) * 2.0 ** -7
+    terms = np.abs(_f64(xd)) @ np.abs(_f64(wd)).T + (np.abs(_f64(rd)) if res else 0.0)
+    bound = ulp + 2.0 ** -20 * terms
+    assert np.all(np.abs(got - want) <= bound), np.abs(got - want).max()
+    assert np.mean(got == want) > 0.95
+
+
+def test_gemm_rows_are_independent_and_deterministic():
+    from paper_2609_04875_amd import gemm_bf16
+    rng = np.random.default_rng(3)
+    x = _bf16_dev(rng.standard_normal((333, 512)))
+    w = _bf16_dev(rng.standard_normal((256, 512)) / 20)
+    full = gemm_bf16(x, w)
+    assert torch.equal(full, gemm_bf16(x, w))
+    part = gemm_bf16(x[101:230].contiguous(), w)
+    assert torch.equal(part, full[101:230])
+
+
+def test_gemm_residual_may_alias_output():
+    from paper_2609_04875_amd import gemm_bf16
+    rng = np.random.default_rng(4)
+    x = _bf16_dev(rng.standard_normal((64, 256)))
+    w = _bf16_dev(rng.standard_normal((128, 256)) / 16)
+    r = _bf16_dev(rng.standard_normal((64, 128)))
+    want = gemm_bf16(x, w, r=r)
+    gemm_bf16(x, w, r=r, out=r)
+    assert torch.equal(r, want)
+
+
+def _small_stack(T=300, dm=1024, layers=3, seed=9):
+    geom = W.AttnGeometry(8, 1, 128)
+    w = W.Workload("small_stack", geom, "bf16", seed=seed, n_layers=layers, d_model=dm, t_total=T)
+    x0, xc, ws = W.stack_inputs(w)
+    return geom, w, x0, xc, ws
+
+
+def test_stack_replay_matches_oracle_and_full_reset():
+    from paper_2609_04875_amd import StackedReplay
+    geom, w, x0, xc, ws = _small_stack()
+    T, P = 300, 203
+    log(f"small stack T={T} P={P}")
+    f32 = lambda b: W.bf16_bits_to_f32(b)
+    wdev = [tuple(_bf16_dev(f32(m).T) for m in layer) for layer in ws]   # [out][in] layout
+    stack = StackedReplay(wdev, geom.n_q_heads, geom.n_kv_heads, geom.head_dim,
+                          n_blocks=2 * (-(-T // 16)) + 8, max_seqs=2, max_blocks_per_seq=32)
+    scale = 128 ** -0.5
+    xs = _bf16_dev(f32(x0))
+    xcont = _bf16_dev(np.concatenate([f32(x0)[:P], f32(xc)[P:]]))
+    stack.replay(0, xcont, scale)                       # contaminated run into the cache
+    assert stack.crop([0], [P]) == 0                    # restore to tau - 1
+    out = stack.replay(0, xs[P:].contiguous(), scale)   # sanitized suffix
+    assert stack.pool.seq_len(0) == T
+    full = stack.full_reset(1, xs, scale)
+    assert torch.equal(full[P:], out)                   # Theorem 1, bitwise
+    # oracle: the sanitized trajectory through the stacked layers
+    layers64 = [tuple(f32(m).astype(np.float64) for m in layer) for layer in ws]
+    ref, _ = oracle.stacked_layers(f32(x0).astype(np.float64), layers64, geom.n_q_heads,
+                                   geom.n_kv_heads, geom.head_dim, scale)
+    # The layer state x is a bf16 residual stream (magnitudes past 8 after three
+    # layers).  GPU and fp64 differ by fp32 accumulation, bf16 P in attention
+    # and storage-rounding flips that later layers carry on; where x + O Wo
+    # cancels to ~0 the elementwise relative error is meaningless.  Bound: two
+    # bf16 ulps at the largest magnitude, and L1-relative error 1e-2.
+    got, want = _f64(out), ref[P:]
+    d = np.abs(got - want)
+    assert d.max() <= 2.0 ** -6 * np.abs(want).max(), (d.max(), np.abs(want).max())
+    assert d.sum() / np.abs(want).sum() <= 1e-2
