@@ -174,6 +174,98 @@ def cpu_baseline(st: Setup, budget_s: float):
                       f"{hq} heads), fp64, {dt:.1f} s incl. crop + reserve on the oracle pool"}
 
 
+def bench_stack(args):
+    """Stacked workload: 8 random-init attention layers (64q/8kv, d 128, d_model
+    8192), T = 16384; for each crop point tau-1 = 25/50/75/95 % of T, crop + replay
+    of the T - tau + 1 sanitized tokens through all layers, against the full
+    reset of all T tokens (Corollary 1: T / (T - tau + 1) fewer transitions)."""
+    import torch
+    import workloads as W
+    from paper_2609_04875_amd import StackedReplay
+
+    w = W.workload("stack70b_8layer_t16384_bf16")
+    g, T, dm = w.geometry, w.t_total, w.d_model
+    x0, xc, layers = W.stack_inputs(w)
+    dev = lambda bits: torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+    wdev = [tuple(dev(np.ascontiguousarray(m.T)) for m in layer) for layer in layers]   # [out][in]
+    del layers
+    x0d, xcd = dev(x0), dev(xc)
+    nbps = -(-T // w.block_size)
+    stack = StackedReplay(wdev, g.n_q_heads, g.n_kv_heads, g.head_dim, n_blocks=2 * nbps + 8,
+                          max_seqs=2, max_blocks_per_seq=nbps + 4)
+    pool = stack.pool
+    scale = w.scale
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, reps):
+        ms = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            ev[0].record()
+            fn()
+            ev[1].record()
+            torch.cuda.synchronize()
+            ms.append(ev[0].elapsed_time(ev[1]))
+        return ms
+
+    gemm_flops_tok = 2.0 * dm * (g.n_q_heads + 2 * g.n_kv_heads) * g.head_dim + 2.0 * g.n_q_heads * g.head_dim * dm
+    full_ms = timed(lambda: stack.full_reset(1, x0d, scale), max(1, args.steps // 4))
+    points = []
+    for frac in w.prefix_fracs:
+        P = int(np.floor(frac * T))
+        S = T - P
+        xcont = torch.cat([x0d[:P], xcd[P:]])
+        pool.crop([0], [0])
+        stack.replay(0, xcont, scale)                # contaminated run into the cache
+        torch.cuda.synchronize()
+        saved = pool.save_meta()
+        xs = x0d[P:].contiguous()
+
+        def step():
+            stack.crop([0], [P])
+            stack.replay(0, xs, scale)
+        ms = []
+        for i in range(args.warmup + max(1, args.steps // 4)):
+            pool.load_meta(saved)
+            m = timed(step, 1)[0]
+            if i >= args.warmup:
+                ms.append(m)
+        attn = sum(attention_flops(P, S, g.n_q_heads, g.head_dim) for _ in range(w.n_layers))
+        gemm = gemm_flops_tok * S * w.n_layers
+        points.append({"prefix": P, "recomputed_tokens": S, "token_ratio": T / S,
+                       "replay_ms": float(np.mean(ms)), "full_reset_ms": float(np.mean(full_ms)),
+                       "wall_time_ratio": float(np.mean(full_ms) / np.mean(ms)),
+                       "replay_flops": attn + gemm,
+                       "replay_TFLOPs": (attn + gemm) / (np.mean(ms) * 1e-3) / 1e12})
+    # kernel times of one layer at the 25 % point, events around each call
+    P = points[0]["prefix"]; S = T - P
+    xs = x0d[P:].contiguous()
+    pool.load_meta(pool.save_meta())
+    wq, wk, wv, wo = stack.w[0]
+    q = torch.empty((S, g.n_q_heads * g.head_dim), dtype=torch.bfloat16, device="cuda")
+    from paper_2609_04875_amd import gemm_bf16
+    gemm_ms = float(np.median(timed(lambda: gemm_bf16(xs, wq, out=q), 5)))
+    gflops = 2.0 * S * dm * g.n_q_heads * g.head_dim
+    total_tokens = sum(p["recomputed_tokens"] for p in points)
+    total_ms = sum(p["replay_ms"] for p in points)
+    result = {
+        "metric": METRIC, "value": total_tokens / (total_ms * 1e-3), "unit": "tokens/s",
+        "n_gpus": 1, "steps": max(1, args.steps // 4), "warmup": args.warmup,
+        "ms_per_step": total_ms / len(points), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "t_total": T, "layers": w.n_layers, "d_model": dm,
+                   "n_q_heads": g.n_q_heads, "n_kv_heads": g.n_kv_heads, "head_dim": g.head_dim,
+                   "prefix_fracs": list(w.prefix_fracs), "block_size": w.block_size},
+        "roofline": {"bound": "mfma", "achieved": gflops / (gemm_ms * 1e-3) / 1e12,
+                     "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
+                     "frac": gflops / (gemm_ms * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"], "traffic": None,
+                     "kernel": "gemm_bf16_kernel (x Wq, S x 8192 x 8192)", "kernel_ms": gemm_ms},
+        "points": points,
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def measured_traffic(workload: str):
     """HBM bytes per attention launch from the committed counter summary
     (FETCH_SIZE, WRITE_SIZE scaled by a plain copy of known size), or None when
@@ -221,6 +313,8 @@ def main() -> int:
     import torch
 
     torch.cuda.set_device(0)
+    if args.workload.startswith("stack"):
+        return bench_stack(args)
     st = Setup(args.workload)
     w, g, pool = st.w, st.w.geometry, st.pool
     single_call = st.calls_per_step == 1
