@@ -253,28 +253,29 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);          // MFMAs
     }
   };
+  // V^T operands of one tile.  The first NVE are read right after the S
+  // products are issued, so their LDS latency overlaps the softmax and the PV
+  // products can start as soon as each 16-key slice of P is ready; the rest
+  // (where registers are short) are read with the PV products.
+  constexpr int NV = KT / 16 * (D / 32);
+  constexpr int NVE = (D == 128 && B > 16) ? 8 : NV;   // wider blocks need more address registers
+  auto read_v = [&](int buf, bf16x8 (&va)[NV], int lo, int hi) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (i >= lo && i < hi)
+        va[i] = __builtin_bit_cast(
+            bf16x8, *(const u32x4*)&v_lds[buf][((i % (D / 32)) * 32 + r) * VLD +
+                                                (i / (D / 32)) * 16 + 8 * hh]);
+  };
   // O^T += V^T P^T for one tile: 16 keys per step.
-  auto pv = [&](int buf, const bf16x8 (&pb)[KT / 16]) {
-    constexpr int N = KT / 16 * (D / 32);
-    bf16x8 va[N];
-#pragma unroll
-    for (int ks = 0; ks < KT / 16; ++ks)
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-        va[ks * (D / 32) + db] = __builtin_bit_cast(
-            bf16x8, *(const u32x4*)&v_lds[buf][(db * 32 + r) * VLD + ks * 16 + 8 * hh]);
+  auto pv = [&](int buf, bf16x8 (&va)[NV], const bf16x8 (&pb)[KT / 16]) {
+    read_v(buf, va, NVE, NV);
 #pragma unroll
     for (int ks = 0; ks < KT / 16; ++ks)
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks * (D / 32) + db], pb[ks],
                                                            oacc[db], 0, 0, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 2);
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      if (i + kAhead < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
-    }
   };
 
   // Prologue: tile kt0 in registers, ids of the next taken, the one after in
@@ -302,6 +303,8 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
     }
     f32x16 s[2];
     qk(buf, s);
+    bf16x8 va[NV];
+    read_v(buf, va, 0, NVE);
     // Causal mask (select) where some key may lie past some row's position.
     if (kb + KT - 1 > first_q) {
 #pragma unroll
@@ -344,7 +347,7 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
     }
-    pv(buf, pb);
+    pv(buf, va, pb);
   }
 
   const float l_tot = l + xor32(l);
