@@ -266,12 +266,19 @@ def bench_stack(args):
     return 0
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per attention launch from the committed counter summary
-    (FETCH_SIZE, WRITE_SIZE scaled by a plain copy of known size), or None when
-    there is none for this workload or the kernel source changed since."""
+def traffic_profile_path(kernel_file: str, workload: str) -> str:
+    """Committed counter summary of the dominant kernel on ``workload``."""
+    short = workload.replace("_bf16", "").replace("_f32", "")
+    return os.path.join(ROOT, "profiles", f"{kernel_file}_{short}_traffic.json")
+
+
+def measured_traffic(kernel_file: str, workload: str):
+    """HBM bytes per step of the dominant kernel (FETCH_SIZE and WRITE_SIZE,
+    each scaled by what it reads for a plain copy of known size), from the
+    committed counter summary; None when there is none for this workload or
+    the kernel source changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"attn_bf16_{workload.replace('_bf16', '')}_traffic.json")
+    path = traffic_profile_path(kernel_file, workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -279,7 +286,7 @@ def measured_traffic(workload: str):
     with open(os.path.join(ROOT, rec["kernel_source"]), "rb") as f:
         if hashlib.sha256(f.read()).hexdigest() != rec["kernel_source_sha256"]:
             return None
-    return rec["traffic_bytes_per_dispatch"]
+    return rec["traffic_bytes_per_step"]
 
 
 def copy_calibration(mib: int) -> None:
@@ -380,7 +387,8 @@ def main() -> int:
                    "head_dim": g.head_dim, "block_size": w.block_size,
                    "recomputed_tokens": sum(st.S)},
         "roofline": {"bound": "mfma" if w.dtype == "bf16" else "alu", "achieved": achieved,
-                     "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": measured_traffic("attn_bf16" if w.dtype == "bf16" else "attn_f32", w.name),
                      "kernel": ("attn_bf16_kernel<128,4,16>" if w.dtype == "bf16"
                                 else f"attn_f32_kernel<{g.head_dim}>"),
                      "flops_per_step": flops, "algorithmic_bytes_per_step": nbytes,
