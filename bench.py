@@ -7,7 +7,8 @@ workload is the 8B attention geometry: 32 query / 8 KV heads, d = 128, bf16, a
 contaminated cache of 10240 tokens cropped to 8189 (not a multiple of the
 16-token block) and a 2048-token suffix replayed against it.  ``--workload``
 selects the other workloads (tiny fp32 episode, 16 ragged episodes in one
-varlen launch, 32k-prefix chunked replay).  Inputs are seeded synthetic
+varlen launch, 32k-prefix chunked replay, the 8-layer stacked workload, and
+``frontend``: the host-side forget queries that produce the crop length).  Inputs are seeded synthetic
 tensors resident in HBM before timing starts.
 
 A crop is destructive, so before every step the pre-crop block table, lengths
@@ -300,6 +301,64 @@ def copy_calibration(mib: int) -> None:
     torch.cuda.synchronize()
 
 
+def bench_frontend(args):
+    """Forget front-end on host cores: the provenance queries and checkpoint
+    choice of Algorithm 1 (locate z's source, first entry tau, taint closure
+    I(z) of Lemma 2, restore point c*) over a long synthetic session recorded
+    in the library's graph, one query per step for a source id drawn in turn.
+    The oracle answers the same queries on the same graph as the CPU baseline."""
+    from workloads import sessions as WS
+    from paper_2609_04875_amd import frontend as F
+    turns, n_ids = 50000, 64
+    recs = WS.draw_session(5, n_turns=turns, per_turn=4, fan_in=3, p_inject=0.05, n_source_ids=n_ids)
+    g = F.ProvenanceGraph(len(recs), sum(len(r[3]) for r in recs), sum(len(r[4]) for r in recs))
+    t0 = time.perf_counter()
+    g.append(recs)
+    append_s = time.perf_counter() - t0
+    store = F.CheckpointStore(turns + 1)
+    for b in g.policy_boundaries("before_injection"):
+        store.register(int(b), g.kv_length_after(int(b)), 0, int(b), int(b))
+    zs = [z for z in range(n_ids) if g.locate_source(z).size]
+    for i in range(args.warmup):
+        F.forget_plan(g, store, zs[i % len(zs)])
+    lat, closure = [], 0
+    for i in range(args.steps):
+        z = zs[i % len(zs)]
+        t0 = time.perf_counter()
+        p = F.forget_plan(g, store, z)
+        lat.append(time.perf_counter() - t0)
+        closure += p.closure_size
+    total = sum(lat)
+    result = {
+        "metric": "forget front-end queries/s (host)", "value": args.steps / total, "unit": "queries/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": total * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": "frontend_session_50k_turns", "artifacts": len(recs),
+                   "edges": sum(len(r[3]) for r in recs), "turns": turns, "source_ids": len(zs),
+                   "checkpoints": len(store), "policy": "before_injection"},
+        "roofline": None,
+        "frontend": {"append_s": append_s, "closure_size_mean": closure / args.steps,
+                     "last_plan": {"tau": p.tau, "boundary": p.boundary, "crop_len": p.crop_len,
+                                   "closure_size": p.closure_size, "replay_transitions": p.replay_transitions,
+                                   "minimal_transitions": p.minimal_transitions}},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import provenance as PV
+        og = PV.ProvenanceGraph()
+        for r in recs:
+            og.append(*r)
+        ocps = PV.checkpoints_for(og, PV.policy_boundaries(og, "before_injection"))
+        t0, n = time.perf_counter(), 0
+        while n < max(1, args.steps) and time.perf_counter() - t0 < args.cpu_seconds:
+            PV.forget_plan(og, ocps, zs[n % len(zs)])
+            n += 1
+        dt = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": n / dt, "unit": "queries/s", "cores": 1, "kind": "oracle",
+                                  "sample": f"{n} queries of the same sequence on the same session"}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -317,6 +376,8 @@ def main() -> int:
                                    "(--gpus must be 1)", "n_gpus": args.gpus}), flush=True)
         return 2
 
+    if args.workload.startswith("frontend"):
+        return bench_frontend(args)
     import torch
 
     torch.cuda.set_device(0)

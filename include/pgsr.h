@@ -60,7 +60,8 @@ enum {
     PGSR_ERANGE = 2,        /* a length outside what the sequence or its table row allows */
     PGSR_ENOMEM = 3,        /* the free list holds too few blocks */
     PGSR_EUNSUPPORTED = 4,  /* a geometry or dtype with no kernel */
-    PGSR_EHIP = 5           /* a HIP runtime call or launch failed */
+    PGSR_EHIP = 5,          /* a HIP runtime call or launch failed */
+    PGSR_ENOENT = 6         /* front-end: the target never entered, or no checkpoint precedes tau */
 };
 
 enum { PGSR_F32 = 0, PGSR_BF16 = 1 };
@@ -182,6 +183,135 @@ int pgsr_pool_last_times(pgsr_pool *pool, float *append_ms, float *attention_ms)
  */
 int pgsr_gemm_bf16(int32_t m, int32_t n, int32_t k, const void *x, const void *w,
                    const void *r, void *y, void *stream);
+
+/* ======================================================================== *
+ * Forget front-end: the provenance queries and checkpoint selection that turn
+ * a forget request for target z into the crop length of the restore
+ * (Algorithm 1, the steps before the restore; Section 3.4 (a) and (b);
+ * Lemma 2; Corollary 1).  Host code only: no device access, no stream.
+ * Handles are not thread-safe; distinct handles may be used concurrently.
+ * Calls validate everything before changing anything (all-or-nothing).
+ *
+ * Readings where the paper is silent:
+ *   turns are 1-indexed; a checkpoint boundary b >= 0 names the state after
+ *   turn b; artifacts arrive in non-decreasing turn order; a parent must
+ *   already exist and belong to the same or an earlier turn (so ids are a
+ *   topological order of the DAG); the artifacts where z enters are those
+ *   whose own source ids contain z, and all of them seed the closure; the KV
+ *   length after turn b is the largest span end over turns <= b; among
+ *   checkpoints with equal boundaries the last registered wins.
+ * ======================================================================== */
+
+/* Artifact types of the recorded data flow (Section 3.4 (a)). */
+enum {
+    PGSR_ART_MEMORY_FIELD = 0, PGSR_ART_PROMPT_BLOCK = 1, PGSR_ART_MODEL_TURN = 2,
+    PGSR_ART_REPLY = 3, PGSR_ART_PLAN = 4, PGSR_ART_TOOL_CALL = 5,
+    PGSR_ART_OBSERVATION = 6, PGSR_ART_SUMMARY = 7
+};
+
+/* Checkpoint placement policies (the granularity ablation of Section 4):
+ * every turn boundary 0..T-1; the session start only; 0 and the boundary
+ * before every turn that introduces a source id; every k-th boundary. */
+enum {
+    PGSR_POLICY_EVERY_TURN = 0, PGSR_POLICY_SESSION_START = 1,
+    PGSR_POLICY_BEFORE_INJECTION = 2, PGSR_POLICY_EVERY_K = 3
+};
+
+typedef struct pgsr_graph pgsr_graph;
+typedef struct pgsr_ckpt_store pgsr_ckpt_store;
+
+/* Result of a forget query (Algorithm 1: locate the source, first entry
+ * boundary, taint closure, restore point c*). */
+typedef struct pgsr_forget_plan {
+    int64_t tau;                  /* first entry boundary: earliest turn where z entered */
+    int64_t checkpoint;           /* index of c* in registration order */
+    int64_t boundary;             /* boundary(c*) < tau */
+    int64_t crop_len;             /* token offset of c*: the length pgsr_kv_crop keeps */
+    int64_t seq;                  /* cache handle (sequence id) of c* */
+    int64_t env_snapshot;         /* environment snapshot id of c* */
+    int64_t manifest;             /* prompt manifest id of c* */
+    int64_t replay_transitions;   /* T - boundary(c*) (Corollary 1) */
+    int64_t minimal_transitions;  /* T - tau + 1 (Corollary 1 lower bound) */
+    int64_t n_sources;            /* artifacts where z entered */
+    int64_t closure_size;         /* |I(z)| (Lemma 2) */
+    int64_t clean_artifacts;      /* |{a : turn(a) < tau}| (Lemma 2 (ii)) */
+    int64_t committed_after_tau;  /* artifacts of turns >= tau with an external side effect */
+} pgsr_forget_plan;
+
+/* Provenance graph G (Section 3.4 (a)) with room for max_artifacts artifacts,
+ * max_edges parent references and max_sources source-id references in total;
+ * all host memory is reserved here.  PGSR_EINVAL on a negative size. */
+int pgsr_graph_create(int64_t max_artifacts, int64_t max_edges, int64_t max_sources,
+                      pgsr_graph **out);
+/* NULL is a no-op. */
+int pgsr_graph_destroy(pgsr_graph *g);
+
+/*
+ * Record n artifacts (ids size .. size+n-1, in order; Lemma 2 (i): G only
+ * grows).  Host arrays of length n: types (PGSR_ART_*), turns (>= 1, not
+ * decreasing, including against the last recorded artifact), span_begin /
+ * span_end (0 <= begin <= end, tokens of the KV timeline), committed (0/1,
+ * may be NULL = none).  Parents of artifact i are parents[parent_off[i] ..
+ * parent_off[i+1]) (parent_off has n+1 entries, starting at 0, not
+ * decreasing); each is an existing id or an earlier one of this batch, of a
+ * turn <= turn[i].  Source ids it introduces: sources[source_off[i] ..
+ * source_off[i+1]), same convention.  parents / sources may be NULL when the
+ * offsets are all 0.  *first_id (may be NULL) receives the first new id.
+ * PGSR_EINVAL on a bad record, PGSR_ENOMEM past the capacity; then nothing is
+ * recorded.
+ */
+int pgsr_graph_append(pgsr_graph *g, int64_t n, const int32_t *types, const int32_t *turns,
+                      const int64_t *span_begin, const int64_t *span_end,
+                      const int64_t *parent_off, const int64_t *parents,
+                      const int64_t *source_off, const int64_t *sources,
+                      const uint8_t *committed, int64_t *first_id);
+
+/* Artifacts recorded; T (the last turn, 0 when empty); tokens in the cache
+ * once turn b is done (b >= 0). */
+int pgsr_graph_size(const pgsr_graph *g, int64_t *n_out);
+int pgsr_graph_session_length(const pgsr_graph *g, int64_t *T_out);
+int pgsr_graph_kv_length_after(const pgsr_graph *g, int64_t b, int64_t *len_out);
+
+/* Locate the source (Algorithm 1): ids of the artifacts where z entered, in
+ * ascending order, into out[0 .. capacity); *n_out = their number.  Returns
+ * PGSR_ERANGE (writing nothing) when capacity is too small; out may be NULL
+ * with capacity 0 to ask for the count. */
+int pgsr_graph_locate_source(const pgsr_graph *g, int64_t z, int64_t *out, int64_t capacity,
+                             int64_t *n_out);
+
+/* Taint closure (Lemma 2): the seeds and every artifact reachable from them,
+ * ascending ids, same output convention as pgsr_graph_locate_source.  Seeds
+ * must be existing ids. */
+int pgsr_graph_taint_closure(const pgsr_graph *g, const int64_t *seeds, int64_t n_seeds,
+                             int64_t *out, int64_t capacity, int64_t *n_out);
+
+/* Boundaries a placement policy yields for the recorded session, ascending,
+ * same output convention; k >= 1 for PGSR_POLICY_EVERY_K (ignored otherwise). */
+int pgsr_graph_policy_boundaries(const pgsr_graph *g, int32_t policy, int64_t k, int64_t *out,
+                                 int64_t capacity, int64_t *n_out);
+
+/* Checkpoint set C (Section 3.4 (b)): metadata only -- the boundary, the token
+ * offset the restore crops to, the cache handle, environment snapshot and
+ * prompt manifest ids; no tensor copies (40 bytes per checkpoint). */
+int pgsr_ckpt_create(int64_t capacity, pgsr_ckpt_store **out);
+int pgsr_ckpt_destroy(pgsr_ckpt_store *s);
+/* PGSR_EINVAL on a negative boundary or offset, PGSR_ENOMEM when full. */
+int pgsr_ckpt_register(pgsr_ckpt_store *s, int64_t boundary, int64_t token_offset, int64_t seq,
+                       int64_t env_snapshot, int64_t manifest);
+int pgsr_ckpt_count(const pgsr_ckpt_store *s, int64_t *n_out);
+
+/*
+ * The forget query of Algorithm 1 for target z: locate where z entered, its
+ * first entry boundary tau, the taint closure I(z), and the restore point
+ * c* = argmax {c : boundary(c) < tau}.  Fills *plan; when closure is not NULL
+ * also writes I(z) (ascending ids) into closure[0 .. capacity).
+ * PGSR_ENOENT when z never entered or no checkpoint lies below tau;
+ * PGSR_ERANGE when capacity < |I(z)| (plan->closure_size is still set, the
+ * closure buffer untouched).  The restore is then pgsr_kv_crop of sequence
+ * plan->seq to plan->crop_len tokens (as int32) on the pool that holds it.
+ */
+int pgsr_forget_plan_query(const pgsr_graph *g, const pgsr_ckpt_store *s, int64_t z,
+                           int64_t *closure, int64_t capacity, pgsr_forget_plan *plan);
 
 #ifdef __cplusplus
 }

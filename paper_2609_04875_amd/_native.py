@@ -14,7 +14,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 # with different compile-time options); the default is the in-tree build.
 LIB_PATH = os.environ.get("PGSR_LIB") or os.path.join(_PKG, "lib", "libpgsr.so")
 
-OK, EINVAL, ERANGE, ENOMEM, EUNSUPPORTED, EHIP = range(6)
+OK, EINVAL, ERANGE, ENOMEM, EUNSUPPORTED, EHIP, ENOENT = range(7)
 F32, BF16 = 0, 1
 COMMIT, POISON = 1, 2
 
@@ -23,7 +23,19 @@ EXPORTS = (
     "pgsr_pool_refresh", "pgsr_seq_len", "pgsr_free_blocks", "pgsr_workspace_bytes",
     "pgsr_kv_crop", "pgsr_replay_prefill", "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
     "pgsr_pool_enable_timing", "pgsr_pool_last_times",
+    "pgsr_graph_create", "pgsr_graph_destroy", "pgsr_graph_append", "pgsr_graph_size",
+    "pgsr_graph_session_length", "pgsr_graph_kv_length_after", "pgsr_graph_locate_source",
+    "pgsr_graph_taint_closure", "pgsr_graph_policy_boundaries", "pgsr_ckpt_create",
+    "pgsr_ckpt_destroy", "pgsr_ckpt_register", "pgsr_ckpt_count", "pgsr_forget_plan_query",
 )
+
+
+class ForgetPlanC(ctypes.Structure):
+    """struct pgsr_forget_plan."""
+    _fields_ = [(name, ctypes.c_int64) for name in (
+        "tau", "checkpoint", "boundary", "crop_len", "seq", "env_snapshot", "manifest",
+        "replay_transitions", "minimal_transitions", "n_sources", "closure_size",
+        "clean_artifacts", "committed_after_tau")]
 
 
 class PgsrError(RuntimeError):
@@ -68,6 +80,26 @@ def _load() -> ctypes.CDLL:
     lib.pgsr_pool_last_times.argtypes = [P, ctypes.POINTER(f32), ctypes.POINTER(f32)]
     lib.pgsr_gemm_bf16.restype = ctypes.c_int
     lib.pgsr_gemm_bf16.argtypes = [i32, i32, i32, P, P, P, P, P]
+    # forget front-end (host only)
+    i64p = ctypes.POINTER(i64)
+    for name, args in (
+            ("pgsr_graph_create", [i64, i64, i64, ctypes.POINTER(P)]),
+            ("pgsr_graph_destroy", [P]),
+            ("pgsr_graph_append", [P, i64, P, P, P, P, P, P, P, P, P, i64p]),
+            ("pgsr_graph_size", [P, i64p]),
+            ("pgsr_graph_session_length", [P, i64p]),
+            ("pgsr_graph_kv_length_after", [P, i64, i64p]),
+            ("pgsr_graph_locate_source", [P, i64, P, i64, i64p]),
+            ("pgsr_graph_taint_closure", [P, P, i64, P, i64, i64p]),
+            ("pgsr_graph_policy_boundaries", [P, i32, i64, P, i64, i64p]),
+            ("pgsr_ckpt_create", [i64, ctypes.POINTER(P)]),
+            ("pgsr_ckpt_destroy", [P]),
+            ("pgsr_ckpt_register", [P, i64, i64, i64, i64, i64]),
+            ("pgsr_ckpt_count", [P, i64p]),
+            ("pgsr_forget_plan_query", [P, P, i64, P, i64, ctypes.POINTER(ForgetPlanC)])):
+        f = getattr(lib, name)
+        f.restype = ctypes.c_int
+        f.argtypes = args
     return lib
 
 

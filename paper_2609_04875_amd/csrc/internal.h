@@ -123,6 +123,10 @@ hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
                             int32_t* free_list, int32_t n_blocks, int32_t* free_top,
                             hipStream_t s);
+// Text returned by pgsr_last_error() on this thread (host runtime).
+void set_error(const char* msg);
+void clear_error();
+
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s);
 

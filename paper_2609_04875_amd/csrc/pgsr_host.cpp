@@ -329,6 +329,12 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
 
 }  // namespace
 
+
+namespace pgsr {
+void set_error(const char* msg) { g_err = msg; }
+void clear_error() { g_err.clear(); }
+}  // namespace pgsr
+
 extern "C" {
 
 const char* pgsr_last_error(void) { return g_err.c_str(); }
