@@ -34,7 +34,10 @@ Readings where the paper is silent:
   P6 checkpoint policies (Section 4 ablation): every_turn places boundaries
      0..T-1; session_start only 0; before_injection places 0 and t-1 for each
      turn t holding an artifact that introduces a source id; every_k places the
-     multiples of k below T.
+     multiples of k below T;
+  P7 execution records artifacts as it goes, so they arrive in non-decreasing
+     turn order; an artifact of an earlier turn than the last one recorded is
+     rejected.
 """
 from __future__ import annotations
 
@@ -63,12 +66,14 @@ class ProvenanceGraph:
     def append(self, type: int, turn: int, span: Tuple[int, int], parents: Sequence[int] = (),
                sources: Iterable[int] = (), committed: bool = False) -> int:
         """Record one artifact; returns its id (ids are 0, 1, 2, ... in order).
-        Invalid records raise ValueError and leave the graph unchanged (P1, P2)."""
+        Invalid records raise ValueError and leave the graph unchanged (P1, P2, P7)."""
         parents = tuple(int(p) for p in parents)
         if not 0 <= type < len(TYPES):
             raise ValueError("unknown artifact type")
         if turn < 1:
             raise ValueError("turns start at 1")
+        if self.artifacts and turn < self.artifacts[-1].turn:
+            raise ValueError("artifacts arrive in turn order")
         if span[0] < 0 or span[1] < span[0]:
             raise ValueError("bad token span")
         for p in parents:

@@ -166,7 +166,7 @@ def test_invalid_appends_change_nothing():
     before = list(g.artifacts)
     for bad in [dict(type=9, turn=2, span=(20, 21)), dict(type=1, turn=0, span=(20, 21)),
                 dict(type=1, turn=2, span=(5, 4)), dict(type=1, turn=2, span=(20, 21), parents=[2]),
-                dict(type=1, turn=1, span=(20, 21), parents=[1])]:
+                dict(type=1, turn=1, span=(20, 21), parents=[1]), dict(type=1, turn=1, span=(20, 21))]:
         with pytest.raises(ValueError):
             g.append(**bad)
         assert g.artifacts == before
