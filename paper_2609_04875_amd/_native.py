@@ -45,6 +45,11 @@ class PgsrError(RuntimeError):
 
 
 def _load() -> ctypes.CDLL:
+    # torch ships its own HIP runtime; it must be the one in the process before
+    # the library is opened, so that both share one runtime (and device memory,
+    # streams and events pass between them).  Opening the library first would
+    # bring in the system runtime alongside torch's.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"{LIB_PATH} is missing: build it with `python paper_2609_04875_amd/build.py` "
