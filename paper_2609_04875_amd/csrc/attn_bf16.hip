@@ -137,6 +137,10 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   const int tok = t0 + w * (32 / G) + r / G;
   const int hq = g * G + r % G;
   const bool valid = tok < e.q_len;
+  // A wave whose 32 rows all lie past the tile's last query (a decode step or
+  // a ragged last tile) still loads and stores its share of every tile but
+  // skips the products.
+  const bool wave_active = __ballot(valid) != 0;
   const int qpos = valid ? e.prefix + tok : -1;
   const int t_last = min(e.q_len, t0 + TW) - 1;
   const int kv_len = e.prefix + e.q_len;
@@ -301,6 +305,7 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
       if (kt + 3 < n_kt) fetch_ids(kt + 3);
       load_tile(ids);
     }
+    if (!wave_active) continue;
     f32x16 s[2];
     qk(buf, s);
     bf16x8 va[NV];
@@ -380,7 +385,12 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
 // s * split_len <= p hold partials (m_s, l_s, acc_s); splits starting past p
 // saw no visible key and may hold stale data, so they are skipped.
 //   M = max m_s,  w_s = 2^(m_s - M),  o = sum_s w_s acc_s / sum_s w_s l_s,
-// summed in increasing s.  16 threads per row, 8 columns each.
+// summed in increasing s.  16 threads per row, 8 columns each.  The partials
+// are read kGroup splits at a time, all loads of a group issued before any is
+// used, so a row with many splits (a decode step) waits on few round trips;
+// the sums still run in increasing s.
+constexpr int kGroup = 8;
+
 template <int D>
 __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t* __restrict__ og) {
   constexpr int TPR = D / 8;                       // threads per row
@@ -394,17 +404,39 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t
   const AttnEntry e = a.e[ei];
   const int qpos = e.prefix + (tok - e.q_off);
   const int ns = min(a.n_splits, qpos / a.split_len + 1);
+  const float* __restrict__ ml = a.ws_ml;
+  const float* __restrict__ acc = a.ws_acc;
+  // Indices past the last split are clamped to it (always a valid address)
+  // and weighted 0, so each group's loads are unconditional and issue together.
   float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ws_ml[2 * ((int64_t)s * a.n_rows + row)]);
+  for (int s0 = 0; s0 < ns; s0 += kGroup) {
+    float mg[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j)
+      mg[j] = ml[2 * ((int64_t)min(s0 + j, ns - 1) * a.n_rows + row)];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) M = fmaxf(M, mg[j]);
+  }
   float L = 0.f;
   f32x4 o0 = {0, 0, 0, 0}, o1 = {0, 0, 0, 0};
-  for (int s = 0; s < ns; ++s) {
-    const int64_t prow = (int64_t)s * a.n_rows + row;
-    const float wgt = __builtin_amdgcn_exp2f(a.ws_ml[2 * prow] - M);
-    L = fmaf(wgt, a.ws_ml[2 * prow + 1], L);
-    const f32x4* acc = (const f32x4*)(a.ws_acc + prow * D + c0);
-    o0 += wgt * acc[0];
-    o1 += wgt * acc[1];
+  for (int s0 = 0; s0 < ns; s0 += kGroup) {
+    float mg[kGroup], lg[kGroup];
+    f32x4 a0[kGroup], a1[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+      const int64_t prow = (int64_t)min(s0 + j, ns - 1) * a.n_rows + row;
+      mg[j] = ml[2 * prow];
+      lg[j] = ml[2 * prow + 1];
+      a0[j] = *(const f32x4*)(acc + prow * D + c0);
+      a1[j] = *(const f32x4*)(acc + prow * D + c0 + 4);
+    }
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+      const float wgt = s0 + j < ns ? __builtin_amdgcn_exp2f(mg[j] - M) : 0.f;
+      L = fmaf(wgt, lg[j], L);
+      o0 += wgt * a0[j];
+      o1 += wgt * a1[j];
+    }
   }
   const float inv = 1.f / L;
   bf16x8 out;

@@ -140,10 +140,11 @@ struct Seg {
 };
 
 // Split-key attention: used when a launch has fewer workgroups than this (two
-// per CU of the 256) and a workspace is available; at most kMaxSplits splits,
+// per CU of the 256) and a workspace is available; at most kMaxSplits splits
+// (a decode step of one sequence, 8 workgroups unsplit, then fills the chip),
 // split boundaries at multiples of the 64-key tile.
 constexpr int64_t kSplitTargetWorkgroups = 512;
-constexpr int64_t kMaxSplits = 16;
+constexpr int64_t kMaxSplits = 32;
 constexpr int32_t kSplitAlign = 64;
 
 // Validation of a replay step: lengths, table width, free blocks.

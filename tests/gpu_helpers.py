@@ -62,11 +62,12 @@ def assert_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "") -
 
 
 def make_pool(geom: W.AttnGeometry, dtype: str, n_blocks: int, max_seqs: int, max_bps: int,
-              n_layers: int = 1, block_size: int = 16, init_free_order=None, split_q: int = 0):
+              n_layers: int = 1, block_size: int = 16, init_free_order=None, split_q: int = 0,
+              max_splits: int = 16):
     """``split_q`` > 0 gives the pool a workspace for split-key replays of up
-    to that many query tokens per call."""
+    to that many query tokens per call, in up to ``max_splits`` splits."""
     from paper_2609_04875_amd import KVPool, F32, BF16, workspace_bytes
-    ws = workspace_bytes(geom.n_q_heads, geom.head_dim, split_q) if split_q else 0
+    ws = workspace_bytes(geom.n_q_heads, geom.head_dim, split_q, max_splits) if split_q else 0
     return KVPool(n_layers, geom.n_q_heads, geom.n_kv_heads, geom.head_dim, n_blocks, max_seqs,
                   max_bps, F32 if dtype == "f32" else BF16, block_size, init_free_order,
                   workspace_bytes=ws)
