@@ -184,6 +184,29 @@ int pgsr_pool_last_times(pgsr_pool *pool, float *append_ms, float *attention_ms)
 int pgsr_gemm_bf16(int32_t m, int32_t n, int32_t k, const void *x, const void *w,
                    const void *r, void *y, void *stream);
 
+/*
+ * Next-token sampling for the re-decode of model-derived suffix content
+ * (Section 3.2, after Lemma 2), deterministic as Theorem 1's assumption A1
+ * asks: the randomness source is fixed by (seed, stream, position).
+ * For row i < n of logits [n][vocab] (device, row-major, dtype PGSR_F32 or
+ * PGSR_BF16):
+ *   temperature > 0: tokens[i] = argmax_v (logits[i][v] / temperature
+ *                     - log(-log u)), scores in fp32, where u for entry v is
+ *                     word (v mod 4) of Philox4x64-10 (Salmon et al., SC 2011)
+ *                     on counter (v div 4, positions[i], streams[i], 0) and
+ *                     key (seed, 0), mapped x -> (floor(x / 2^41) + 1/2) / 2^23;
+ *   temperature == 0: tokens[i] = argmax_v logits[i][v] (greedy).
+ * Ties go to the lowest index; NaN scores never win.  streams, positions: host
+ * int64 arrays of n; tokens: device int32 [n].  With a device workspace of at
+ * least pgsr_sample_workspace_bytes(n, vocab) bytes the vocabulary is split
+ * over several workgroups per row (same result); workspace may be NULL.
+ * PGSR_EINVAL on a bad size, pointer or temperature (negative, NaN, inf).
+ */
+size_t pgsr_sample_workspace_bytes(int32_t n, int32_t vocab);
+int pgsr_sample_tokens(int32_t n, int32_t vocab, int32_t dtype, const void *logits, float temperature,
+                       uint64_t seed, const int64_t *streams, const int64_t *positions, void *workspace,
+                       size_t workspace_bytes, int32_t *tokens, void *stream);
+
 /* ======================================================================== *
  * Forget front-end: the provenance queries and checkpoint selection that turn
  * a forget request for target z into the crop length of the restore

@@ -12,9 +12,10 @@ length) is host code in the same library.
 from ._native import (BF16, COMMIT, EHIP, EINVAL, ENOENT, ENOMEM, EUNSUPPORTED, ERANGE, F32, OK,
                       POISON, PgsrError)
 from .frontend import CheckpointStore, ForgetPlan, ProvenanceGraph, forget_plan
+from .sampling import sample_tokens, sample_workspace_bytes
 from .pool import KVPool, gemm_bf16, workspace_bytes
 from .stack import StackedReplay
 
 __all__ = ["KVPool", "StackedReplay", "gemm_bf16", "workspace_bytes", "ProvenanceGraph", "CheckpointStore",
-           "ForgetPlan", "forget_plan", "PgsrError", "OK", "EINVAL", "ERANGE", "ENOMEM", "EUNSUPPORTED",
+           "ForgetPlan", "forget_plan", "sample_tokens", "sample_workspace_bytes", "PgsrError", "OK", "EINVAL", "ERANGE", "ENOMEM", "EUNSUPPORTED",
            "EHIP", "ENOENT", "F32", "BF16", "COMMIT", "POISON"]

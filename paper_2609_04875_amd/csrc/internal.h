@@ -109,6 +109,25 @@ struct AttnArgs {
   AttnEntry e[kMaxSeqsPerLaunch];
 };
 
+// ------------------------------------------------------------- sampling -- //
+struct SampleArgs {
+  int32_t n;           // rows in this launch
+  int32_t row0;        // first row of this launch in logits / tokens
+  int32_t vocab;
+  int32_t n_chunks;    // workgroups per row; > 1 writes partial keys
+  int32_t chunk_len;   // vocabulary entries per chunk, a multiple of 4
+  float temperature;   // 0: greedy
+  uint64_t seed;
+  uint64_t* partial;   // [rows][n_chunks] keys when n_chunks > 1
+  int64_t stream[kMaxSeqsPerLaunch];
+  int64_t position[kMaxSeqsPerLaunch];
+};
+
+hipError_t launch_sample(const SampleArgs& a, int dtype, const void* logits, int32_t* tokens,
+                         hipStream_t s);
+hipError_t launch_sample_reduce(int32_t n, int32_t n_chunks, const uint64_t* partial, int32_t* tokens,
+                                hipStream_t s);
+
 // Query tokens per workgroup tile for each kernel (the host sizes grids with these).
 int attn_f32_tile_tokens(int head_dim, int group);
 int attn_bf16_tile_tokens(int head_dim, int group);

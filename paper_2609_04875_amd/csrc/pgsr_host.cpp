@@ -578,4 +578,50 @@ int pgsr_gemm_bf16(int32_t m, int32_t n, int32_t k, const void* x, const void* w
   return ok();
 }
 
+// Vocabulary entries per sampling workgroup (a multiple of 4: Philox blocks
+// never straddle two chunks).
+constexpr int32_t kSampleChunk = 8192;
+
+size_t pgsr_sample_workspace_bytes(int32_t n, int32_t vocab) {
+  if (n <= 0 || vocab <= kSampleChunk) return 0;
+  return (size_t)n * (size_t)cdiv(vocab, kSampleChunk) * sizeof(uint64_t);
+}
+
+int pgsr_sample_tokens(int32_t n, int32_t vocab, int32_t dtype, const void* logits, float temperature,
+                       uint64_t seed, const int64_t* streams, const int64_t* positions, void* workspace,
+                       size_t workspace_bytes, int32_t* tokens, void* stream) {
+  if (n < 0 || vocab <= 0) return fail(PGSR_EINVAL, "n = %d, vocab = %d", n, vocab);
+  if (dtype != PGSR_F32 && dtype != PGSR_BF16) return fail(PGSR_EUNSUPPORTED, "dtype %d", dtype);
+  if (!(temperature >= 0.f) || temperature > 3.0e38f)
+    return fail(PGSR_EINVAL, "temperature must be finite and >= 0");
+  if (n == 0) return ok();
+  if (!logits || !tokens || !streams || !positions) return fail(PGSR_EINVAL, "null pointer");
+  const int32_t chunks = cdiv(vocab, kSampleChunk);
+  const bool split = chunks > 1 && workspace &&
+                     workspace_bytes >= (size_t)n * (size_t)chunks * sizeof(uint64_t);
+  hipStream_t st = (hipStream_t)stream;
+  SampleArgs a{};
+  a.vocab = vocab;
+  a.n_chunks = split ? chunks : 1;
+  a.chunk_len = split ? kSampleChunk : ((vocab + 3) / 4) * 4;
+  a.temperature = temperature;
+  a.seed = seed;
+  a.partial = split ? (uint64_t*)workspace : nullptr;
+  for (int32_t r0 = 0; r0 < n; r0 += kMaxSeqsPerLaunch) {
+    a.row0 = r0;
+    a.n = std::min<int32_t>(kMaxSeqsPerLaunch, n - r0);
+    for (int32_t i = 0; i < a.n; ++i) {
+      a.stream[i] = streams[r0 + i];
+      a.position[i] = positions[r0 + i];
+    }
+    hipError_t err = launch_sample(a, dtype, logits, tokens, st);
+    if (err != hipSuccess) return hip_fail(err, "sample launch");
+  }
+  if (split) {
+    hipError_t err = launch_sample_reduce(n, chunks, (const uint64_t*)workspace, tokens, st);
+    if (err != hipSuccess) return hip_fail(err, "sample reduce launch");
+  }
+  return ok();
+}
+
 }  // extern "C"
