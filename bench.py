@@ -7,8 +7,9 @@ workload is the 8B attention geometry: 32 query / 8 KV heads, d = 128, bf16, a
 contaminated cache of 10240 tokens cropped to 8189 (not a multiple of the
 16-token block) and a 2048-token suffix replayed against it.  ``--workload``
 selects the other workloads (tiny fp32 episode, 16 ragged episodes in one
-varlen launch, 32k-prefix chunked replay, the 8-layer stacked workload, and
-``frontend``: the host-side forget queries that produce the crop length).  Inputs are seeded synthetic
+varlen launch, 32k-prefix chunked replay, the 8-layer stacked workload,
+``decode``: one-token steps over 32 cached sequences with seeded sampling,
+and ``frontend``: the host-side forget queries that produce the crop length).  Inputs are seeded synthetic
 tensors resident in HBM before timing starts.
 
 A crop is destructive, so before every step the pre-crop block table, lengths
@@ -301,6 +302,88 @@ def copy_calibration(mib: int) -> None:
     torch.cuda.synchronize()
 
 
+def bench_decode(args):
+    """Re-decode of model-derived suffix content (Section 3.2 after Lemma 2):
+    32 sequences with 8192-token caches (8B geometry, bf16), one token per
+    sequence per step: reserve + append, split-key decode attention over the
+    whole cache, then seeded Gumbel-max sampling (T = 0.7) over a 128256-entry
+    vocabulary of synthetic logits (the LM head is not on this path).  The
+    roofline is HBM: K/V bytes one step must read over the attention time."""
+    import torch
+    from paper_2609_04875_amd import BF16, KVPool, sample_tokens, sample_workspace_bytes, workspace_bytes
+    n, ctx, hq, hkv, d, B, vocab, T = 32, 8192, 32, 8, 128, 16, 128256, 0.7
+    total = args.warmup + args.steps
+    bps = (ctx + total) // B + 2
+    pool = KVPool(1, hq, hkv, d, n * bps + 8, n, bps, BF16, B, workspace_bytes=workspace_bytes(hq, d, n, 32))
+    g = torch.Generator(device="cuda").manual_seed(7)
+    rnd = lambda *shape: torch.randn(*shape, device="cuda", generator=g).to(torch.bfloat16)
+    keep = None
+    for s in range(n):
+        q, k, v = rnd(ctx, hq, d), rnd(ctx, hkv, d), rnd(ctx, hkv, d)
+        assert pool.replay(0, [s], [ctx], q, k, v, torch.empty_like(q), d ** -0.5) == 0
+        if s == 0:
+            keep = (k.float().cpu().numpy().astype(np.float64), v.float().cpu().numpy().astype(np.float64))
+    qs, ks, vs = rnd(total, n, hq, d), rnd(total, n, hkv, d), rnd(total, n, hkv, d)
+    logits = rnd(n, vocab)
+    o = torch.empty(n, hq, d, dtype=torch.bfloat16, device="cuda")
+    tokens = torch.empty(n, dtype=torch.int32, device="cuda")
+    sws = torch.empty(max(sample_workspace_bytes(n, vocab), 1), dtype=torch.uint8, device="cuda")
+    seqs = list(range(n))
+    pool.enable_timing(True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    step_ms, attn_ms, samp_ms, kv_bytes = [], [], [], []
+    torch.cuda.synchronize()
+    for t in range(total):
+        ev[0].record()
+        assert pool.replay(0, seqs, [1] * n, qs[t], ks[t], vs[t], o, d ** -0.5) == 0
+        ev[1].record()
+        sample_tokens(logits, T, 1234, seqs, [ctx + t] * n, out=tokens, workspace=sws)
+        ev[2].record()
+        torch.cuda.synchronize()
+        if t >= args.warmup:
+            step_ms.append(ev[0].elapsed_time(ev[2]))
+            samp_ms.append(ev[1].elapsed_time(ev[2]))
+            attn_ms.append(pool.last_times()[1])
+            kv_bytes.append(n * (ctx + t + 1) * hkv * d * 2 * 2 + 2 * n * hq * d * 2)
+    if args.calibrate_copy_mib:
+        copy_calibration(args.calibrate_copy_mib)
+    a_ms = float(np.mean(attn_ms))
+    achieved = float(np.mean(kv_bytes)) / (a_ms * 1e-3) / 1e9
+    total_s = sum(step_ms) / 1e3
+    result = {
+        "metric": "decode tokens/s (split-key paged attention + seeded sampling)", "value": n * args.steps / total_s,
+        "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": total_s * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "decode_llama8b_b32_ctx8192", "sequences": n, "context": ctx,
+                   "n_q_heads": hq, "n_kv_heads": hkv, "head_dim": d, "block_size": B, "vocab": vocab,
+                   "temperature": T},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": 8000.0, "unit": "GB/s",
+                     "frac": achieved / 8000.0,
+                     "traffic": measured_traffic("attn_bf16", "decode_llama8b_b32_ctx8192"),
+                     "kernel": "attn_bf16_kernel<128,4,16> + split_combine_kernel<128>",
+                     "kernel_ms": a_ms, "kernel_launches_per_step": 1,
+                     "algorithmic_bytes_per_step": float(np.mean(kv_bytes))},
+        "breakdown_ms": {"attention": a_ms, "sampling": float(np.mean(samp_ms)),
+                         "step": total_s * 1e3 / args.steps},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        k0, v0 = keep
+        q0 = qs[0, 0:1].float().cpu().numpy().astype(np.float64)      # a decode row at position ctx
+        kk = np.concatenate([k0, ks[0, 0:1].float().cpu().numpy().astype(np.float64)])
+        vv = np.concatenate([v0, vs[0, 0:1].float().cpu().numpy().astype(np.float64)])
+        t0, m = time.perf_counter(), 0
+        while m == 0 or time.perf_counter() - t0 < min(args.cpu_seconds, 10.0):
+            oracle.attention(q0, kk, vv, ctx, d ** -0.5)
+            m += 1
+        dt = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": m / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+                                  "sample": f"{m} decode rows of one sequence (all 32 heads, 8193 keys)"}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def bench_frontend(args):
     """Forget front-end on host cores: the provenance queries and checkpoint
     choice of Algorithm 1 (locate z's source, first entry tau, taint closure
@@ -383,6 +466,8 @@ def main() -> int:
     torch.cuda.set_device(0)
     if args.workload.startswith("stack"):
         return bench_stack(args)
+    if args.workload.startswith("decode"):
+        return bench_decode(args)
     st = Setup(args.workload)
     w, g, pool = st.w, st.w.geometry, st.pool
     single_call = st.calls_per_step == 1
