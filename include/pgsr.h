@@ -88,7 +88,9 @@ int pgsr_abi_version(void);
  * not touched.  workspace (device, nullable) is scratch for split-key partial
  * results, workspace_bytes long (see pgsr_workspace_bytes); NULL disables
  * key splitting.  Supported: dtype PGSR_F32 or PGSR_BF16, head_dim 64 or 128,
- * block_size 16, 32 or 64, n_q_heads a multiple of n_kv_heads.  Blocks.
+ * block_size 16, 32 or 64, n_q_heads a multiple of n_kv_heads (bf16: at
+ * most 32 query heads per KV head, any such group, e.g. 7 for 28 / 4
+ * heads).  Blocks.
  */
 int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                      int32_t block_size, int32_t dtype, int32_t n_blocks, int32_t max_seqs,

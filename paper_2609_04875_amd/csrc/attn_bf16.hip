@@ -127,16 +127,19 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   while (ei + 1 < a.n && a.e[ei + 1].tile_start <= tile) ++ei;
   const AttnEntry e = a.e[ei];
   const int G = a.n_q_heads / hkv;
-  const int TW = NW * 32 / G;                       // tokens per tile
+  // A wave holds TPW = floor(32 / G) tokens x G heads; when G does not divide
+  // 32 (e.g. 7) its last 32 - TPW * G rows are padding and never written.
+  const int TPW = 32 / G;
+  const int TW = NW * TPW;                          // tokens per tile
   const int n_tiles_e = (e.q_len + TW - 1) / TW;
   const int lt = n_tiles_e - 1 - (tile - e.tile_start);
   const int t0 = lt * TW;
 
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, r = lane & 31, hh = lane >> 5;
-  const int tok = t0 + w * (32 / G) + r / G;
+  const int tok = t0 + w * TPW + r / G;
   const int hq = g * G + r % G;
-  const bool valid = tok < e.q_len;
+  const bool valid = r < TPW * G && tok < e.q_len;
   // A wave whose 32 rows all lie past the tile's last query (a decode step or
   // a ragged last tile) still loads and stores its share of every tile but
   // skips the products.
@@ -450,7 +453,7 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t
 
 }  // namespace
 
-int attn_bf16_tile_tokens(int, int group) { return kNW * 32 / group; }
+int attn_bf16_tile_tokens(int, int group) { return kNW * (32 / group); }
 
 template <int D, int B>
 static void launch_d_b(const AttnArgs& a, hipStream_t s) {

@@ -362,8 +362,8 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
   if (block_size != 16 && block_size != 32 && block_size != 64)
     return fail(PGSR_EUNSUPPORTED, "block_size %d (supported: 16, 32, 64)", block_size);
   const int group = n_q_heads / n_kv_heads;
-  if (dtype == PGSR_BF16 && (32 % group != 0))
-    return fail(PGSR_EUNSUPPORTED, "bf16 kernels need n_q_heads / n_kv_heads to divide 32");
+  if (dtype == PGSR_BF16 && group > 32)
+    return fail(PGSR_EUNSUPPORTED, "bf16 kernels need n_q_heads / n_kv_heads <= 32");
   if ((int64_t)max_seqs * max_blocks_per_seq > INT32_MAX)
     return fail(PGSR_ERANGE, "block table larger than 2^31-1 entries");
   if (!k_cache || !v_cache || !block_tables || !seq_lens || !free_list || !free_top)

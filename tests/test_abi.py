@@ -55,7 +55,7 @@ def test_create_rejects_bad_geometry_before_any_device_call(native):
     assert create(d=96) == native.EUNSUPPORTED
     assert create(B=8) == native.EUNSUPPORTED
     assert create(hq=30) == native.EUNSUPPORTED
-    assert create(hq=24, hkv=8) == native.EUNSUPPORTED       # group 3 does not divide 32 (bf16)
+    assert create(hq=33, hkv=1) == native.EUNSUPPORTED       # bf16: at most 32 query heads per KV head
     assert create(dt=7) == native.EUNSUPPORTED
     assert create(nb=0) == native.EINVAL
     order = native.int32_array([0, 1, 1] + list(range(3, 64)))

@@ -60,6 +60,10 @@ GEOMS = [
     (64, 8, 128, 100, 33),
     (16, 2, 128, 47, 200),
     (4, 4, 128, 64, 64),
+    # groups that do not divide 32: padded rows in every wave
+    (28, 4, 128, 333, 101),      # the Qwen2.5-7B geometry, G = 7
+    (24, 8, 128, 95, 60),        # G = 3
+    (20, 4, 64, 17, 41),         # G = 5, d = 64
 ]
 
 
@@ -88,6 +92,20 @@ def test_bf16_selective_equals_full_reset_bitwise_and_deterministic():
     assert torch.equal(o1, o2)                                  # (A1) determinism
     full = _full_reset(pool, ep, 1, scale)
     assert torch.equal(full[ep.prefix:], o1)                    # Theorem 1, bitwise
+
+
+def test_group7_selective_equals_full_reset_bitwise():
+    """Theorem 1 at G = 7 (28 query / 4 KV heads): the padded rows change nothing."""
+    geom = W.AttnGeometry(28, 4, 128)
+    rng = np.random.default_rng(77)
+    ep = W.draw_episode(rng, geom, "bf16", 1003, 250, 1300)
+    scale = 128 ** -0.5
+    pool = make_pool(geom, "bf16", 2 * _blocks(1300) + 8, 2, 128)
+    contaminated_then_crop(pool, ep, 0, scale)
+    o = _replay(pool, ep, 0, scale, commit=False)
+    full = _full_reset(pool, ep, 1, scale)
+    assert torch.equal(full[ep.prefix:], o)
+    assert_close(o.float().cpu().numpy(), oracle_suffix(ep, scale), "bf16", "G=7")
 
 
 def test_earlier_clean_boundary_is_equally_exact():

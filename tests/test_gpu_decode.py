@@ -16,6 +16,7 @@ pytestmark = pytest.mark.gpu
 
 GEOM = W.AttnGeometry(32, 8, 128)
 SCALE = 128 ** -0.5
+GEOM7 = W.AttnGeometry(28, 4, 128)
 
 
 def _blocks(n, B=16):
@@ -70,6 +71,21 @@ def test_decode_steps_match_oracle(prefixes):
             for name, o in zip(("split", "plain"), outs):
                 assert_close(o[t, s:s + 1].float().cpu().numpy(), ref, "bf16", f"{name} step {t} seq {s}")
     assert not torch.equal(outs[0], outs[1])       # the split path was taken
+
+
+def test_decode_group7():
+    """Decode at the Qwen2.5-7B geometry (28 / 4 heads, G = 7)."""
+    rng = np.random.default_rng(70)
+    prefixes, steps = (2000, 45), 3
+    eps = [W.draw_episode(rng, GEOM7, "bf16", P, steps, P + steps) for P in prefixes]
+    nb = sum(_blocks(P + steps) + 1 for P in prefixes) + 4
+    pool = make_pool(GEOM7, "bf16", nb, 2, _blocks(2003) + 1, split_q=2, max_splits=64)
+    for s, ep in enumerate(eps):
+        _prefill(pool, ep, s)
+    out = _decode(pool, eps, [0, 1], steps)
+    for t in range(steps):
+        for s, ep in enumerate(eps):
+            assert_close(out[t, s:s + 1].float().cpu().numpy(), _oracle_step(ep, t), "bf16", f"G7 {t} {s}")
 
 
 def test_decode_is_bitwise_reproducible():
