@@ -28,7 +28,17 @@ Readings where the paper is silent (it never describes paging):
      no-op, a crop to 0 frees every block; duplicates / out-of-range are errors
      and change nothing (all-or-nothing);
   R4 a reservation pops, per sequence in call order, the blocks for logical
-     indices nalloc .. ceil((len + S) / B) - 1 in increasing order.
+     indices nalloc .. ceil((len + S) / B) - 1 in increasing order;
+  R5 copy-on-write fork (all methods branch from one contaminated base,
+     Section 4.1): a fork gives an empty sequence the source's table row and
+     length, and every block counts the table entries that name it.  A crop
+     releases an entry by decrementing its block's count and pushes the block
+     only when the count reaches 0 (same order as R3).  A reservation that
+     would write into a partial tail block (len mod B != 0, S > 0) named by more
+     than one entry first pops a private block, copies the tail block's first
+     len mod B slots of every layer into it, and puts it in the row (the old
+     block's count drops by 1); this pop comes before the R4 pops.  Without
+     forks every count is 0 or 1 and R3/R4 are unchanged.
 """
 from __future__ import annotations
 
@@ -141,6 +151,7 @@ class PoolModel:
     nalloc [max_seqs]              blocks held per row (>= ceil(len/B); larger
                                    while a reserved replay step is uncommitted)
     free   [n_blocks]              stack storage; free[0 .. top) are free ids (R2)
+    refs   [n_blocks]              table entries naming each block (R5)
     """
 
     def __init__(self, n_blocks: int, max_seqs: int, max_blocks: int, block_size: int,
@@ -158,6 +169,7 @@ class PoolModel:
             if sorted(self.free.tolist()) != list(range(n_blocks)):
                 raise ValueError("init_free_order must be a permutation of the block ids")
         self.top = n_blocks
+        self.refs = np.zeros(n_blocks, np.int32)
         # optional data: [layer][block][slot][kv_head][d], fp64 (oracle's own layout)
         self.kdata = self.vdata = None
         if n_layers:
@@ -187,11 +199,41 @@ class PoolModel:
         for s, L in zip(seqs, new_lens):
             keep = _cdiv(L, self.B)
             for j in range(keep, int(self.nalloc[s])):       # ascending logical order (R3)
-                self.free[self.top] = self.tables[s, j]
-                self.top += 1
+                b = int(self.tables[s, j])
                 self.tables[s, j] = -1
+                self.refs[b] -= 1
+                if self.refs[b] == 0:                         # last entry naming it (R5)
+                    self.free[self.top] = b
+                    self.top += 1
             self.nalloc[s] = keep
             self.lens[s] = L
+        return OK
+
+    def _shared_tail(self, s: int, S: int) -> bool:
+        """R5: the next write lands in a partial tail block other entries name."""
+        L = int(self.lens[s])
+        return S > 0 and L % self.B != 0 and int(self.refs[self.tables[s, L // self.B]]) > 1
+
+    def fork(self, srcs: Sequence[int], dsts: Sequence[int]) -> int:
+        """Copy-on-write fork (R5): each empty dsts[i] shares srcs[i]'s blocks."""
+        if len(srcs) != len(dsts):
+            return EINVAL
+        for ids in (srcs, dsts):
+            for x in ids:
+                if not (0 <= x < self.tables.shape[0]):
+                    return EINVAL
+        if len(set(dsts)) != len(dsts) or set(dsts) & set(srcs):
+            return EINVAL
+        for d in dsts:
+            if self.lens[d] != 0 or self.nalloc[d] != 0:
+                return EINVAL
+        for s, d in zip(srcs, dsts):
+            n = int(self.nalloc[s])
+            self.tables[d, :n] = self.tables[s, :n]
+            self.nalloc[d] = n
+            self.lens[d] = self.lens[s]
+            for b in self.tables[s, :n]:
+                self.refs[b] += 1
         return OK
 
     def reserve(self, seqs: Sequence[int], q_lens: Sequence[int]) -> int:
@@ -209,12 +251,27 @@ class PoolModel:
             if blocks > self.tables.shape[1]:
                 return ERANGE
             need.append(max(0, blocks - int(self.nalloc[s])))
-        if sum(need) > self.top:
+        cow = [self._shared_tail(s, S) for s, S in zip(seqs, q_lens)]
+        if sum(need) + sum(cow) > self.top:
             return ENOMEM
-        for s, n in zip(seqs, need):
+        for s, n, c in zip(seqs, need, cow):
+            if c:                                             # private copy of the tail block (R5)
+                j = int(self.lens[s]) // self.B
+                old = int(self.tables[s, j])
+                self.top -= 1
+                new = int(self.free[self.top])
+                if self.kdata is not None:
+                    t = int(self.lens[s]) % self.B
+                    self.kdata[:, new, :t] = self.kdata[:, old, :t]
+                    self.vdata[:, new, :t] = self.vdata[:, old, :t]
+                self.tables[s, j] = new
+                self.refs[old] -= 1
+                self.refs[new] = 1
             for _ in range(n):
                 self.top -= 1
-                self.tables[s, self.nalloc[s]] = self.free[self.top]
+                b = int(self.free[self.top])
+                self.tables[s, self.nalloc[s]] = b
+                self.refs[b] = 1
                 self.nalloc[s] += 1
         return OK
 
@@ -242,7 +299,7 @@ class PoolModel:
 
     def state(self) -> Dict[str, np.ndarray]:
         return {"tables": self.tables.copy(), "lens": self.lens.copy(),
-                "free": self.free.copy(), "top": np.int32(self.top)}
+                "free": self.free.copy(), "top": np.int32(self.top), "refs": self.refs.copy()}
 
 
 def prefill(pool: PoolModel, layer: int, seqs: Sequence[int], q_lens: Sequence[int],
