@@ -29,8 +29,10 @@
  *   seq_lens     int32 [max_seqs]          committed tokens per sequence
  *   free_list    int32 [n_blocks]          LIFO stack of free block ids
  *   free_top     int32 [1]                 stack height
+ *   ref_counts   int32 [n_blocks]          table entries naming each block
  * Logical token p of sequence s lives in block block_tables[s][p / B] at
- * slot p % B.  A sequence's slots at or beyond its length hold unspecified
+ * slot p % B.  Rows may share blocks after pgsr_kv_fork (copy-on-write): a
+ * block is free exactly when its count is 0.  A sequence's slots at or beyond its length hold unspecified
  * data (possibly NaN) and are never read.
  *
  * Errors.  Every call returns a status.  Arguments are validated against the
@@ -81,8 +83,8 @@ int pgsr_abi_version(void);
 
 /*
  * Create a pool over caller-owned device memory and initialise its device
- * state: every table entry -1, every length 0, free_list = the initial stack,
- * free_top = n_blocks.  init_free_order (HOST, nullable, n_blocks entries) is
+ * state: every table entry -1, every length 0, every count 0, free_list = the
+ * initial stack, free_top = n_blocks.  init_free_order (HOST, nullable, n_blocks entries) is
  * the stack from bottom to top and must be a permutation of 0 .. n_blocks-1;
  * NULL means n_blocks-1 .. 0, so pops yield 0, 1, 2, ....  The KV caches are
  * not touched.  workspace (device, nullable) is scratch for split-key partial
@@ -96,16 +98,17 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
                      int32_t block_size, int32_t dtype, int32_t n_blocks, int32_t max_seqs,
                      int32_t max_blocks_per_seq, void *k_cache, void *v_cache,
                      int32_t *block_tables, int32_t *seq_lens, int32_t *free_list,
-                     int32_t *free_top, void *workspace, size_t workspace_bytes,
-                     const int32_t *init_free_order, void *stream, pgsr_pool **out);
+                     int32_t *free_top, int32_t *ref_counts, void *workspace,
+                     size_t workspace_bytes, const int32_t *init_free_order, void *stream,
+                     pgsr_pool **out);
 
 /* Release the host object; device memory is the caller's. NULL is a no-op. */
 int pgsr_pool_destroy(pgsr_pool *pool);
 
 /* Re-read the host mirror from device state (blocking).  For callers that
- * restore block_tables / seq_lens / free_list / free_top themselves, e.g. by
- * copying a saved pre-crop state back; a row's block count is taken as the
- * number of leading non-negative entries. */
+ * restore block_tables / seq_lens / free_list / free_top / ref_counts
+ * themselves, e.g. by copying a saved pre-crop state back; a row's block count
+ * is taken as the number of leading non-negative entries. */
 int pgsr_pool_refresh(pgsr_pool *pool, void *stream);
 
 /* Host-mirror queries (no device access). */
@@ -121,9 +124,10 @@ size_t pgsr_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int64_t max_tot
  * Restore = crop (Algorithm 1, restore step; Section 3.4 (b); Lemma 1): for
  * each i, keep the first new_lens[i] tokens of sequence seqs[i]
  * (0 <= new_lens[i] <= its length).  Table entries from ceil(new_len / B) on
- * become -1 and those block ids are pushed onto the free list, sequences in
- * call order, ascending logical block within a sequence; a crop to the current
- * length is a no-op and a crop to 0 releases every block.  KV data of the kept
+ * become -1 and each such block's count drops by 1; blocks whose count reaches
+ * 0 are pushed onto the free list, sequences in call order, ascending logical
+ * block within a sequence (without forks every released block is pushed); a
+ * crop to the current length is a no-op and a crop to 0 releases every entry.  KV data of the kept
  * tokens is not touched.  seqs and new_lens are HOST arrays of n entries; a
  * duplicate sequence is PGSR_EINVAL.  flags: 0 or PGSR_POISON.
  * All-or-nothing.
@@ -132,11 +136,26 @@ int pgsr_kv_crop(pgsr_pool *pool, int32_t n, const int32_t *seqs, const int32_t 
                  unsigned flags, void *stream);
 
 /*
+ * Copy-on-write fork (every method branches from the same contaminated base,
+ * Section 4.1): for each i, the EMPTY sequence dsts[i] (length 0, no blocks)
+ * takes the table row and length of srcs[i]; no KV data moves, and each shared
+ * block's count grows by 1.  Later crops of either row release only their own
+ * references, and the first write into a shared partial tail block copies it
+ * (see pgsr_replay_prefill).  srcs, dsts: HOST arrays of n; a target that is
+ * not empty, appears twice or is also a source is PGSR_EINVAL.  All-or-nothing.
+ */
+int pgsr_kv_fork(pgsr_pool *pool, int32_t n, const int32_t *srcs, const int32_t *dsts,
+                 void *stream);
+
+/*
  * One layer of F over the sanitized suffix, prefill form (Algorithm 1, replay
  * loop; Theorem 1; re-materialisation by prefill, Section 3.2 after Lemma 2).
  * For each i, with P_i the committed length of seqs[i] and S_i = q_lens[i]:
  *   1. blocks for positions P_i .. P_i+S_i-1 are popped from the free list when
- *      the row holds fewer (so the first layer of a step reserves them);
+ *      the row holds fewer (so the first layer of a step reserves them); if
+ *      the partial tail block (P_i mod B != 0) is shared with another row, a
+ *      private block is popped first and receives its slots 0 .. P_i mod B - 1
+ *      of every layer (copy-on-write; the shared block's count drops by 1);
  *   2. the S_i new keys/values are written to positions P_i .. P_i+S_i-1 of
  *      `layer` (filling the partial tail block first);
  *   3. o receives, for the query at absolute position p = P_i + t and query

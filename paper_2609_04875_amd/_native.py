@@ -21,7 +21,7 @@ COMMIT, POISON = 1, 2
 EXPORTS = (
     "pgsr_last_error", "pgsr_abi_version", "pgsr_pool_create", "pgsr_pool_destroy",
     "pgsr_pool_refresh", "pgsr_seq_len", "pgsr_free_blocks", "pgsr_workspace_bytes",
-    "pgsr_kv_crop", "pgsr_replay_prefill", "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
+    "pgsr_kv_crop", "pgsr_kv_fork", "pgsr_replay_prefill", "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
     "pgsr_pool_enable_timing", "pgsr_pool_last_times",
     "pgsr_graph_create", "pgsr_graph_destroy", "pgsr_graph_append", "pgsr_graph_size",
     "pgsr_graph_session_length", "pgsr_graph_kv_length_after", "pgsr_graph_locate_source",
@@ -62,8 +62,10 @@ def _load() -> ctypes.CDLL:
     lib.pgsr_last_error.argtypes = []
     lib.pgsr_abi_version.restype = ctypes.c_int
     lib.pgsr_pool_create.restype = ctypes.c_int
-    lib.pgsr_pool_create.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P, P,
+    lib.pgsr_pool_create.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P, P, P,
                                      ctypes.c_size_t, i32p, P, ctypes.POINTER(P)]
+    lib.pgsr_kv_fork.restype = ctypes.c_int
+    lib.pgsr_kv_fork.argtypes = [P, i32, i32p, i32p, P]
     lib.pgsr_pool_destroy.restype = ctypes.c_int
     lib.pgsr_pool_destroy.argtypes = [P]
     lib.pgsr_pool_refresh.restype = ctypes.c_int

@@ -19,23 +19,27 @@ struct CropEntry {
   int32_t new_len;   // tokens kept
   int32_t keep;      // ceil(new_len / B): table entries kept
   int32_t nalloc;    // entries held before the crop
-  int32_t push_off;  // where this sequence's freed ids start above top_before
+  int32_t tail_private;  // poison only: the kept partial block is named by this row alone
 };
 
+// One workgroup takes the entries in call order; each released table entry
+// decrements its block's count, and blocks reaching 0 are pushed in ascending
+// entry order starting at top_before.
 struct CropArgs {
   int32_t* tables;
   int32_t* lens;
   int32_t* free_list;
   int32_t* free_top;
+  int32_t* refs;
   int32_t max_bps;
   int32_t top_before;  // stack height when this launch starts
-  int32_t top_after;   // stack height when this launch ends
   int32_t n;
   CropEntry e[kMaxSeqsPerLaunch];
 };
 
-// Debug aid: NaN-fill every slot a crop released (freed blocks in all layers,
-// and the tail slots of a kept partial block).
+// Debug aid: NaN-fill every slot a crop released: whole blocks it pushed
+// (free_list[top_before .. top_before + n_freed)) in all layers, and the tail
+// slots of a kept partial block that no other row names.
 struct PoisonArgs {
   void* k_cache;
   void* v_cache;
@@ -43,8 +47,25 @@ struct PoisonArgs {
   const int32_t* free_list;
   int32_t max_bps, n_layers, n_blocks, n_kv_heads, block_size, head_dim, elem_bytes;
   int32_t top_before;
+  int32_t n_freed;
   int32_t n;
   CropEntry e[kMaxSeqsPerLaunch];
+};
+
+// --------------------------------------------------------------- fork ----- //
+struct ForkEntry {
+  int32_t src, dst;
+  int32_t nalloc;   // table entries of src, shared with dst
+  int32_t len;      // tokens of src
+};
+
+struct ForkArgs {
+  int32_t* tables;
+  int32_t* lens;
+  int32_t* refs;
+  int32_t max_bps;
+  int32_t n;
+  ForkEntry e[kMaxSeqsPerLaunch];
 };
 
 // --------------------------------------------------------- reserve+append - //
@@ -57,6 +78,8 @@ struct AppendEntry {
   int32_t stack_before;   // stack height before this sequence's pops
   int32_t lb_first;       // first logical block touched: P / B
   int32_t item_start;     // prefix sum of logical blocks touched over entries
+  int32_t cow_old;        // shared partial tail block to copy before writing, or -1;
+                          // its private copy is the first block popped for this entry
 };
 
 struct AppendArgs {
@@ -68,7 +91,8 @@ struct AppendArgs {
   int32_t* lens;
   const int32_t* free_list;
   int32_t* free_top;
-  int32_t max_bps, n_blocks, n_kv_heads, block_size, head_dim, layer;
+  int32_t* refs;
+  int32_t max_bps, n_blocks, n_kv_heads, block_size, head_dim, layer, n_layers;
   int32_t commit;
   int32_t write_top;   // 1: this launch writes free_top = top_after
   int32_t top_after;
@@ -134,13 +158,14 @@ int attn_bf16_tile_tokens(int head_dim, int group);
 
 hipError_t launch_crop(const CropArgs& a, hipStream_t s);
 hipError_t launch_poison(const PoisonArgs& a, hipStream_t s);
+hipError_t launch_fork(const ForkArgs& a, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 // Merge split-key partials into O (bf16), splits in increasing order.
 hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
-                            int32_t* free_list, int32_t n_blocks, int32_t* free_top,
+                            int32_t* free_list, int32_t n_blocks, int32_t* free_top, int32_t* refs,
                             hipStream_t s);
 // Text returned by pgsr_last_error() on this thread (host runtime).
 void set_error(const char* msg);

@@ -1,6 +1,9 @@
 // Paged KV pool kernels: initial state, restore-by-crop (block-table truncation
 // and compaction of the released ids onto the free-list stack), NaN poisoning
-// of released slots, and the reserve + append step of a replay.
+// of released slots, copy-on-write fork, and the reserve + append step of a
+// replay.  Every block carries a count of the table entries that name it: a
+// crop pushes a block only when its count reaches 0, and an append that would
+// write into a shared partial tail block first copies it into a private one.
 //
 // All of this is integer bookkeeping and bit copies: results are exact and do
 // not depend on the launch shape.  Work per call is tiny (a crop touches at
@@ -16,33 +19,70 @@ namespace {
 
 __global__ void __launch_bounds__(256)
 pool_init_kernel(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
-                 int32_t* free_list, int32_t n_blocks, int32_t* free_top) {
+                 int32_t* free_list, int32_t n_blocks, int32_t* free_top, int32_t* refs) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_table; i += stride)
     tables[i] = -1;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < max_seqs; i += stride)
     lens[i] = 0;
-  if (free_list)  // default stack: bottom n_blocks-1 ... top 0, so pops yield 0, 1, 2, ...
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_blocks; i += stride)
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_blocks; i += stride) {
+    refs[i] = 0;
+    if (free_list)  // default stack: bottom n_blocks-1 ... top 0, so pops yield 0, 1, 2, ...
       free_list[i] = n_blocks - 1 - (int32_t)i;
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0) *free_top = n_blocks;
 }
 
-// One workgroup per cropped sequence.  Entries j >= keep of the row move onto
-// the stack at top_before + push_off + (j - keep), in ascending j.
+// One workgroup takes the entries in call order (a block named by two of the
+// cropped rows must reach 0 in the later one).  Within a row the released
+// entries j = keep .. nalloc-1 name distinct blocks, so 256 of them are
+// decremented at once; those reaching 0 are pushed in ascending j through a
+// prefix count over the workgroup.
 __global__ void __launch_bounds__(256) crop_kernel(CropArgs a) {
-  const CropEntry e = a.e[blockIdx.x];
-  int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
-  const int32_t n_free = e.nalloc - e.keep;
-  int32_t* dst = a.free_list + a.top_before + e.push_off;
-  for (int32_t j = threadIdx.x; j < n_free; j += blockDim.x) {
-    dst[j] = row[e.keep + j];
-    row[e.keep + j] = -1;
+  __shared__ int32_t wave_cnt[4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int32_t top = a.top_before;
+  for (int i = 0; i < a.n; ++i) {
+    const CropEntry e = a.e[i];
+    int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
+    for (int32_t j0 = e.keep; j0 < e.nalloc; j0 += 256) {
+      const int32_t j = j0 + (int32_t)threadIdx.x;
+      bool freed = false;
+      int32_t b = -1;
+      if (j < e.nalloc) {
+        b = row[j];
+        row[j] = -1;
+        const int32_t r = a.refs[b] - 1;
+        a.refs[b] = r;
+        freed = r == 0;
+      }
+      const uint64_t m = __ballot(freed);
+      if (lane == 0) wave_cnt[w] = __popcll(m);
+      __syncthreads();
+      int32_t before = __popcll(m & ((1ull << lane) - 1ull));
+      for (int ww = 0; ww < w; ++ww) before += wave_cnt[ww];
+      const int32_t total = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+      if (freed) a.free_list[top + before] = b;
+      top += total;
+      __syncthreads();   // wave_cnt is reused; count writes precede the next row's reads
+    }
+    if (threadIdx.x == 0) a.lens[e.seq] = e.new_len;
   }
-  if (threadIdx.x == 0) {
-    a.lens[e.seq] = e.new_len;
-    if (blockIdx.x == 0) *a.free_top = a.top_after;
+  if (threadIdx.x == 0) *a.free_top = top;
+}
+
+// One workgroup per pair: dst (empty) takes src's row and length; every shared
+// block's count grows by 1 (atomics: several pairs may share a source).
+__global__ void __launch_bounds__(256) fork_kernel(ForkArgs a) {
+  const ForkEntry e = a.e[blockIdx.x];
+  const int32_t* src = a.tables + (int64_t)e.src * a.max_bps;
+  int32_t* dst = a.tables + (int64_t)e.dst * a.max_bps;
+  for (int32_t j = threadIdx.x; j < e.nalloc; j += blockDim.x) {
+    const int32_t b = src[j];
+    dst[j] = b;
+    atomicAdd(&a.refs[b], 1);
   }
+  if (threadIdx.x == 0) a.lens[e.dst] = e.len;
 }
 
 template <typename T>
@@ -50,22 +90,24 @@ __device__ void fill_nan(T* p, int64_t n, T nan, int tid, int nthreads) {
   for (int64_t i = tid; i < n; i += nthreads) p[i] = nan;
 }
 
-// blockIdx.x: entry; blockIdx.y: layer.  Runs after crop_kernel on the same stream.
+// blockIdx.x < n_freed: a pushed block; above: a cropped entry's tail slots
+// (private kept partial blocks only).  blockIdx.y: layer.  Runs after
+// crop_kernel on the same stream.
 template <typename T>
 __global__ void __launch_bounds__(256) poison_kernel(PoisonArgs a, T nan) {
-  const CropEntry e = a.e[blockIdx.x];
   const int layer = blockIdx.y;
   const int64_t blk_elems = (int64_t)a.n_kv_heads * a.block_size * a.head_dim;
   T* kc = (T*)a.k_cache + (int64_t)layer * a.n_blocks * blk_elems;
   T* vc = (T*)a.v_cache + (int64_t)layer * a.n_blocks * blk_elems;
-  const int32_t n_free = e.nalloc - e.keep;
-  for (int32_t j = 0; j < n_free; ++j) {
-    const int32_t id = a.free_list[a.top_before + e.push_off + j];
+  if ((int)blockIdx.x < a.n_freed) {
+    const int32_t id = a.free_list[a.top_before + blockIdx.x];
     fill_nan(kc + (int64_t)id * blk_elems, blk_elems, nan, threadIdx.x, blockDim.x);
     fill_nan(vc + (int64_t)id * blk_elems, blk_elems, nan, threadIdx.x, blockDim.x);
+    return;
   }
+  const CropEntry e = a.e[blockIdx.x - a.n_freed];
   const int32_t tail = e.new_len % a.block_size;
-  if (tail != 0) {  // slots tail .. B-1 of the kept partial block
+  if (tail != 0 && e.tail_private) {  // slots tail .. B-1 of the kept partial block
     const int32_t id = a.tables[(int64_t)e.seq * a.max_bps + e.keep - 1];
     const int B = a.block_size, D = a.head_dim;
     const int per_head = (B - tail) * D;
@@ -74,6 +116,39 @@ __global__ void __launch_bounds__(256) poison_kernel(PoisonArgs a, T nan) {
       const int slot = tail + r / D, c = r % D;
       kc[(int64_t)id * blk_elems + ((int64_t)h * B + slot) * D + c] = nan;
       vc[(int64_t)id * blk_elems + ((int64_t)h * D + c) * B + slot] = nan;
+    }
+  }
+}
+
+// Copy-on-write before an append: for an entry whose next write lands in a
+// shared partial tail block (cow_old), the first block popped for it becomes
+// the row's private copy of slots 0 .. P mod B - 1 of every layer (this
+// workgroup: one KV head).  Launched before append_kernel on the same stream,
+// so every copy has read the shared block before any entry of the call writes
+// into it (a later entry may own that block outright once this one has left).
+template <typename T>
+__global__ void __launch_bounds__(256) cow_kernel(AppendArgs a) {
+  const AppendEntry e = a.e[blockIdx.x];
+  if (e.cow_old < 0) return;
+  const int B = a.block_size, D = a.head_dim, h = blockIdx.y;
+  const int32_t id = a.free_list[e.stack_before - 1];
+  const int s0 = e.prefix - e.lb_first * B;
+  if (h == 0 && threadIdx.x == 0) {
+    a.tables[(int64_t)e.seq * a.max_bps + e.lb_first] = id;
+    a.refs[id] = 1;
+    atomicSub(&a.refs[e.cow_old], 1);   // rows of several entries may share it
+  }
+  for (int L = 0; L < a.n_layers; ++L) {
+    const int64_t ob = ((int64_t)L * a.n_blocks + e.cow_old) * a.n_kv_heads + h;
+    const int64_t nb = ((int64_t)L * a.n_blocks + id) * a.n_kv_heads + h;
+    const T* ko = (const T*)a.k_cache + ob * B * D;
+    const T* vo = (const T*)a.v_cache + ob * D * B;
+    T* kn = (T*)a.k_cache + nb * B * D;
+    T* vn = (T*)a.v_cache + nb * D * B;
+    for (int i = threadIdx.x; i < s0 * D; i += blockDim.x) kn[i] = ko[i];   // K: [slot][d]
+    for (int i = threadIdx.x; i < D * s0; i += blockDim.x) {                // V: [d][slot]
+      const int c = i / s0, t = i % s0;
+      vn[(int64_t)c * B + t] = vo[(int64_t)c * B + t];
     }
   }
 }
@@ -95,12 +170,16 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
   const int B = a.block_size, D = a.head_dim, h = blockIdx.y;
   const int32_t lb = e.lb_first + (item - e.item_start);
   int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
+  const int32_t cow_pops = e.cow_old >= 0 ? 1 : 0;   // cow_kernel took the first pop
   int32_t id;
   if (lb < e.nalloc_before) {
     id = row[lb];
   } else {
-    id = a.free_list[e.stack_before - 1 - (lb - e.nalloc_before)];
-    if (h == 0 && threadIdx.x == 0) row[lb] = id;
+    id = a.free_list[e.stack_before - 1 - cow_pops - (lb - e.nalloc_before)];
+    if (h == 0 && threadIdx.x == 0) {
+      row[lb] = id;
+      a.refs[id] = 1;
+    }
   }
   if (threadIdx.x == 0 && h == 0) {
     if (a.commit && item == e.item_start) a.lens[e.seq] = e.prefix + e.q_len;
@@ -131,7 +210,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
 }  // namespace
 
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
-                            int32_t* free_list, int32_t n_blocks, int32_t* free_top,
+                            int32_t* free_list, int32_t n_blocks, int32_t* free_top, int32_t* refs,
                             hipStream_t s) {
   int64_t biggest = n_table > n_blocks ? n_table : n_blocks;
   if (max_seqs > biggest) biggest = max_seqs;
@@ -139,29 +218,42 @@ hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int
   if (grid > 4096) grid = 4096;
   if (grid < 1) grid = 1;
   hipLaunchKernelGGL(pool_init_kernel, dim3(grid), dim3(256), 0, s, tables, n_table, lens,
-                     max_seqs, free_list, n_blocks, free_top);
+                     max_seqs, free_list, n_blocks, free_top, refs);
   return hipGetLastError();
 }
 
 hipError_t launch_crop(const CropArgs& a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(crop_kernel, dim3(a.n), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(crop_kernel, dim3(1), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fork(const ForkArgs& a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fork_kernel, dim3(a.n), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_poison(const PoisonArgs& a, hipStream_t s) {
-  if (a.n <= 0) return hipSuccess;
+  if (a.n + a.n_freed <= 0) return hipSuccess;
+  const dim3 grid(a.n_freed + a.n, a.n_layers);
   if (a.elem_bytes == 4)
-    hipLaunchKernelGGL(poison_kernel<uint32_t>, dim3(a.n, a.n_layers), dim3(256), 0, s, a,
-                       (uint32_t)0x7FC00000u);
+    hipLaunchKernelGGL(poison_kernel<uint32_t>, grid, dim3(256), 0, s, a, (uint32_t)0x7FC00000u);
   else
-    hipLaunchKernelGGL(poison_kernel<uint16_t>, dim3(a.n, a.n_layers), dim3(256), 0, s, a,
-                       (uint16_t)0x7FC0u);
+    hipLaunchKernelGGL(poison_kernel<uint16_t>, grid, dim3(256), 0, s, a, (uint16_t)0x7FC0u);
   return hipGetLastError();
 }
 
 hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s) {
   if (a.n <= 0 || a.n_items <= 0) return hipSuccess;
+  bool any_cow = false;
+  for (int i = 0; i < a.n; ++i) any_cow |= a.e[i].cow_old >= 0;
+  if (any_cow) {
+    if (elem_bytes == 4)
+      hipLaunchKernelGGL(cow_kernel<uint32_t>, dim3(a.n, a.n_kv_heads), dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(cow_kernel<uint16_t>, dim3(a.n, a.n_kv_heads), dim3(256), 0, s, a);
+  }
   dim3 grid(a.n_items, a.n_kv_heads);
   if (elem_bytes == 4)
     hipLaunchKernelGGL(append_kernel<uint32_t>, grid, dim3(256), 0, s, a);

@@ -27,10 +27,15 @@ struct pgsr_pool {
   int32_t* lens;
   int32_t* free_list;
   int32_t* free_top;
+  int32_t* refs;
   void* workspace;
   size_t workspace_bytes;
-  // host mirror
+  // host mirror of the metadata, updated at call time in enqueue order by the
+  // same steps the kernels take
   std::vector<int32_t> h_len, h_nalloc;
+  std::vector<int32_t> h_tab;    // [max_seqs][max_bps]
+  std::vector<int32_t> h_free;   // stack storage
+  std::vector<int32_t> h_ref;    // table entries naming each block
   int32_t h_top;
   // optional kernel timing: events around the append and attention launches
   bool timing = false, timed_call = false;
@@ -78,9 +83,48 @@ int check_seqs(const pgsr_pool* p, int32_t n, const int32_t* seqs) {
 }
 
 // ------------------------------------------------------------------ crop -- //
+// Mirror of a crop of sequence s to L tokens: released entries, ascending,
+// decrement their block's count; blocks reaching 0 are pushed.
+void mirror_crop(pgsr_pool* p, int32_t s, int32_t L) {
+  const int32_t keep = cdiv(L, p->B);
+  int32_t* row = &p->h_tab[(size_t)s * p->max_bps];
+  for (int32_t j = keep; j < p->h_nalloc[s]; ++j) {
+    const int32_t b = row[j];
+    row[j] = -1;
+    if (--p->h_ref[b] == 0) p->h_free[p->h_top++] = b;
+  }
+  p->h_nalloc[s] = keep;
+  p->h_len[s] = L;
+}
+
+// Blocks a crop of these sequences would push (the mirror is left unchanged).
+int64_t count_freed(const pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_lens) {
+  std::vector<std::pair<int32_t, int32_t>> dec;   // (block, decrements so far)
+  int64_t freed = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = seqs[i], keep = cdiv(new_lens[i], p->B);
+    for (int32_t j = keep; j < p->h_nalloc[s]; ++j) {
+      const int32_t b = p->h_tab[(size_t)s * p->max_bps + j];
+      int32_t k = 0;
+      for (auto& d : dec)
+        if (d.first == b) k = ++d.second;
+      if (k == 0) dec.push_back({b, k = 1});
+      if (p->h_ref[b] - k == 0) ++freed;
+    }
+  }
+  return freed;
+}
+
+// Does the next write of sequence s (prefix P, S > 0 tokens) land in a partial
+// tail block that other table entries also name?
+bool shared_tail(const pgsr_pool* p, int32_t s, int32_t P, int32_t S) {
+  if (S <= 0 || P % p->B == 0) return false;
+  const int32_t b = p->h_tab[(size_t)s * p->max_bps + P / p->B];
+  return b >= 0 && p->h_ref[b] > 1;
+}
+
 int do_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_lens,
             unsigned flags, hipStream_t st) {
-  int32_t top = p->h_top;
   for (int32_t base = 0; base < n; base += kMaxSeqsPerLaunch) {
     const int32_t cnt = std::min<int32_t>(kMaxSeqsPerLaunch, n - base);
     CropArgs a{};
@@ -88,10 +132,10 @@ int do_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_len
     a.lens = p->lens;
     a.free_list = p->free_list;
     a.free_top = p->free_top;
+    a.refs = p->refs;
     a.max_bps = p->max_bps;
-    a.top_before = top;
+    a.top_before = p->h_top;
     a.n = cnt;
-    int32_t off = 0;
     for (int32_t i = 0; i < cnt; ++i) {
       const int32_t s = seqs[base + i], L = new_lens[base + i];
       CropEntry& e = a.e[i];
@@ -99,10 +143,10 @@ int do_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_len
       e.new_len = L;
       e.keep = cdiv(L, p->B);
       e.nalloc = p->h_nalloc[s];
-      e.push_off = off;
-      off += e.nalloc - e.keep;
+      mirror_crop(p, s, L);
+      const int32_t tb = e.keep > 0 ? p->h_tab[(size_t)s * p->max_bps + e.keep - 1] : -1;
+      e.tail_private = tb >= 0 && p->h_ref[tb] == 1;
     }
-    a.top_after = top + off;
     hipError_t err = launch_crop(a, st);
     if (err != hipSuccess) return hip_fail(err, "crop launch");
     if (flags & PGSR_POISON) {
@@ -118,18 +162,13 @@ int do_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_len
       pa.block_size = p->B;
       pa.head_dim = p->d;
       pa.elem_bytes = elem_bytes(p);
-      pa.top_before = top;
+      pa.top_before = a.top_before;
+      pa.n_freed = p->h_top - a.top_before;
       pa.n = cnt;
       std::memcpy(pa.e, a.e, sizeof(CropEntry) * cnt);
       err = launch_poison(pa, st);
       if (err != hipSuccess) return hip_fail(err, "poison launch");
     }
-    for (int32_t i = 0; i < cnt; ++i) {
-      p->h_nalloc[a.e[i].seq] = a.e[i].keep;
-      p->h_len[a.e[i].seq] = a.e[i].new_len;
-    }
-    top = a.top_after;
-    p->h_top = top;
   }
   return PGSR_OK;
 }
@@ -164,6 +203,7 @@ int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* se
       return fail(PGSR_ERANGE, "sequence %d would reach %lld tokens; its row holds %lld",
                   seqs[i], (long long)end, (long long)p->max_bps * p->B);
     need += std::max<int64_t>(0, cdiv(end, p->B) - nalloc[i]);
+    if (nalloc[i] > 0 && shared_tail(p, seqs[i], prefix[i], S)) ++need;   // private tail copy
     total += S;
   }
   if (total > INT32_MAX) return fail(PGSR_ERANGE, "more than 2^31-1 query tokens in one call");
@@ -194,8 +234,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     hipError_t err = hipEventRecord(p->ev[0], st);
     if (err != hipSuccess) return hip_fail(err, "timing event");
   }
-  // Reserve + append, chunked.
-  int32_t top = p->h_top;
+  // Reserve + append, chunked; the mirror takes the same pops in call order.
   for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
     const int32_t cnt = (int32_t)std::min<size_t>(kMaxSeqsPerLaunch, segs.size() - base);
     AppendArgs a{};
@@ -207,42 +246,51 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.lens = p->lens;
     a.free_list = p->free_list;
     a.free_top = p->free_top;
+    a.refs = p->refs;
     a.max_bps = p->max_bps;
     a.n_blocks = p->n_blocks;
     a.n_kv_heads = p->hkv;
     a.block_size = p->B;
     a.head_dim = p->d;
     a.layer = layer;
+    a.n_layers = p->n_layers;
     a.commit = commit ? 1 : 0;
     a.n = cnt;
     int32_t items = 0;
     for (int32_t i = 0; i < cnt; ++i) {
       const Seg& g = segs[base + i];
       AppendEntry& e = a.e[i];
+      int32_t* row = &p->h_tab[(size_t)g.seq * p->max_bps];
       e.seq = g.seq;
       e.prefix = g.prefix;
       e.q_len = g.q_len;
       e.q_off = g.q_off;
       e.nalloc_before = p->h_nalloc[g.seq];
-      e.stack_before = top;
+      e.stack_before = p->h_top;
       e.lb_first = g.prefix / p->B;
       e.item_start = items;
+      e.cow_old = -1;
       const int32_t end_blocks = cdiv((int64_t)g.prefix + g.q_len, p->B);
       items += end_blocks - e.lb_first;
-      const int32_t pops = std::max(0, end_blocks - e.nalloc_before);
-      top -= pops;
+      if (shared_tail(p, g.seq, g.prefix, g.q_len)) {   // private copy first
+        e.cow_old = row[e.lb_first];
+        const int32_t nb = p->h_free[--p->h_top];
+        --p->h_ref[e.cow_old];
+        p->h_ref[nb] = 1;
+        row[e.lb_first] = nb;
+      }
+      for (int32_t lb = p->h_nalloc[g.seq]; lb < end_blocks; ++lb) {
+        const int32_t nb = p->h_free[--p->h_top];
+        p->h_ref[nb] = 1;
+        row[lb] = nb;
+      }
+      p->h_nalloc[g.seq] = std::max(p->h_nalloc[g.seq], end_blocks);
     }
     a.n_items = items;
     a.write_top = 1;
-    a.top_after = top;
+    a.top_after = p->h_top;
     hipError_t err = launch_append(a, eb, st);
     if (err != hipSuccess) return hip_fail(err, "append launch");
-    for (int32_t i = 0; i < cnt; ++i) {
-      const Seg& g = segs[base + i];
-      p->h_nalloc[g.seq] =
-          std::max(p->h_nalloc[g.seq], cdiv((int64_t)g.prefix + g.q_len, p->B));
-    }
-    p->h_top = top;
   }
 
   if (p->timing) {
@@ -340,14 +388,15 @@ extern "C" {
 
 const char* pgsr_last_error(void) { return g_err.c_str(); }
 
-int pgsr_abi_version(void) { return 1; }
+int pgsr_abi_version(void) { return 2; }
 
 int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                      int32_t block_size, int32_t dtype, int32_t n_blocks, int32_t max_seqs,
                      int32_t max_blocks_per_seq, void* k_cache, void* v_cache,
                      int32_t* block_tables, int32_t* seq_lens, int32_t* free_list,
-                     int32_t* free_top, void* workspace, size_t workspace_bytes,
-                     const int32_t* init_free_order, void* stream, pgsr_pool** out) {
+                     int32_t* free_top, int32_t* ref_counts, void* workspace,
+                     size_t workspace_bytes, const int32_t* init_free_order, void* stream,
+                     pgsr_pool** out) {
   if (!out) return fail(PGSR_EINVAL, "out is null");
   *out = nullptr;
   if (n_layers <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_blocks <= 0 || max_seqs <= 0 ||
@@ -366,7 +415,7 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
     return fail(PGSR_EUNSUPPORTED, "bf16 kernels need n_q_heads / n_kv_heads <= 32");
   if ((int64_t)max_seqs * max_blocks_per_seq > INT32_MAX)
     return fail(PGSR_ERANGE, "block table larger than 2^31-1 entries");
-  if (!k_cache || !v_cache || !block_tables || !seq_lens || !free_list || !free_top)
+  if (!k_cache || !v_cache || !block_tables || !seq_lens || !free_list || !free_top || !ref_counts)
     return fail(PGSR_EINVAL, "null device pointer");
   if (workspace == nullptr) workspace_bytes = 0;
   if (init_free_order) {
@@ -381,7 +430,7 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
   hipStream_t st = (hipStream_t)stream;
   hipError_t err = launch_pool_init(block_tables, (int64_t)max_seqs * max_blocks_per_seq,
                                     seq_lens, max_seqs, init_free_order ? nullptr : free_list,
-                                    n_blocks, free_top, st);
+                                    n_blocks, free_top, ref_counts, st);
   if (err != hipSuccess) return hip_fail(err, "pool init launch");
   if (init_free_order) {
     err = hipMemcpyAsync(free_list, init_free_order, sizeof(int32_t) * n_blocks,
@@ -406,10 +455,16 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
   p->lens = seq_lens;
   p->free_list = free_list;
   p->free_top = free_top;
+  p->refs = ref_counts;
   p->workspace = workspace;
   p->workspace_bytes = workspace_bytes;
   p->h_len.assign(max_seqs, 0);
   p->h_nalloc.assign(max_seqs, 0);
+  p->h_tab.assign((size_t)max_seqs * max_blocks_per_seq, -1);
+  p->h_free.resize(n_blocks);
+  for (int32_t i = 0; i < n_blocks; ++i)
+    p->h_free[i] = init_free_order ? init_free_order[i] : n_blocks - 1 - i;
+  p->h_ref.assign(n_blocks, 0);
   p->h_top = n_blocks;
   *out = p;
   return ok();
@@ -450,23 +505,37 @@ int pgsr_pool_refresh(pgsr_pool* p, void* stream) {
   if (!p) return fail(PGSR_EINVAL, "pool is null");
   hipStream_t st = (hipStream_t)stream;
   std::vector<int32_t> tables((size_t)p->max_seqs * p->max_bps), lens(p->max_seqs);
+  std::vector<int32_t> free_list(p->n_blocks), refs(p->n_blocks);
   int32_t top = 0;
   hipError_t err = hipMemcpyAsync(tables.data(), p->tables, tables.size() * 4,
                                   hipMemcpyDeviceToHost, st);
   if (err == hipSuccess)
     err = hipMemcpyAsync(lens.data(), p->lens, lens.size() * 4, hipMemcpyDeviceToHost, st);
+  if (err == hipSuccess)
+    err = hipMemcpyAsync(free_list.data(), p->free_list, free_list.size() * 4, hipMemcpyDeviceToHost, st);
+  if (err == hipSuccess)
+    err = hipMemcpyAsync(refs.data(), p->refs, refs.size() * 4, hipMemcpyDeviceToHost, st);
   if (err == hipSuccess) err = hipMemcpyAsync(&top, p->free_top, 4, hipMemcpyDeviceToHost, st);
   if (err == hipSuccess) err = hipStreamSynchronize(st);
   if (err != hipSuccess) return hip_fail(err, "refresh copy");
   if (top < 0 || top > p->n_blocks) return fail(PGSR_ERANGE, "device free_top %d invalid", top);
+  std::vector<int32_t> nalloc(p->max_seqs);
   for (int32_t s = 0; s < p->max_seqs; ++s) {
     int32_t na = 0;
     while (na < p->max_bps && tables[(size_t)s * p->max_bps + na] >= 0) ++na;
     if (lens[s] < 0 || cdiv(lens[s], p->B) > na)
       return fail(PGSR_ERANGE, "device length %d of sequence %d exceeds its blocks", lens[s], s);
-    p->h_nalloc[s] = na;
-    p->h_len[s] = lens[s];
+    for (int32_t j = 0; j < na; ++j)
+      if (tables[(size_t)s * p->max_bps + j] >= p->n_blocks)
+        return fail(PGSR_ERANGE, "device table of sequence %d names block %d", s,
+                    tables[(size_t)s * p->max_bps + j]);
+    nalloc[s] = na;
   }
+  p->h_nalloc = nalloc;
+  p->h_len = lens;
+  p->h_tab = tables;
+  p->h_free = free_list;
+  p->h_ref = refs;
   p->h_top = top;
   return ok();
 }
@@ -508,6 +577,48 @@ int pgsr_kv_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* ne
   return rc ? rc : ok();
 }
 
+int pgsr_kv_fork(pgsr_pool* p, int32_t n, const int32_t* srcs, const int32_t* dsts, void* stream) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
+  if (n == 0) return ok();
+  if (!srcs || !dsts) return fail(PGSR_EINVAL, "null srcs / dsts");
+  int rc = check_seqs(p, n, dsts);
+  if (rc) return rc;
+  std::vector<char> is_dst(p->max_seqs, 0);
+  for (int32_t i = 0; i < n; ++i) is_dst[dsts[i]] = 1;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = srcs[i], d = dsts[i];
+    if (s < 0 || s >= p->max_seqs) return fail(PGSR_EINVAL, "source sequence id %d", s);
+    if (is_dst[s]) return fail(PGSR_EINVAL, "sequence %d is both a source and a target", s);
+    if (p->h_len[d] != 0 || p->h_nalloc[d] != 0)
+      return fail(PGSR_EINVAL, "target sequence %d is not empty", d);
+  }
+  hipStream_t st = (hipStream_t)stream;
+  for (int32_t base = 0; base < n; base += kMaxSeqsPerLaunch) {
+    const int32_t cnt = std::min<int32_t>(kMaxSeqsPerLaunch, n - base);
+    ForkArgs a{};
+    a.tables = p->tables;
+    a.lens = p->lens;
+    a.refs = p->refs;
+    a.max_bps = p->max_bps;
+    a.n = cnt;
+    for (int32_t i = 0; i < cnt; ++i) {
+      const int32_t s = srcs[base + i], d = dsts[base + i];
+      a.e[i] = {s, d, p->h_nalloc[s], p->h_len[s]};
+      for (int32_t j = 0; j < p->h_nalloc[s]; ++j) {
+        const int32_t b = p->h_tab[(size_t)s * p->max_bps + j];
+        p->h_tab[(size_t)d * p->max_bps + j] = b;
+        ++p->h_ref[b];
+      }
+      p->h_nalloc[d] = p->h_nalloc[s];
+      p->h_len[d] = p->h_len[s];
+    }
+    hipError_t err = launch_fork(a, st);
+    if (err != hipSuccess) return hip_fail(err, "fork launch");
+  }
+  return ok();
+}
+
 int pgsr_replay_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
                         const int32_t* q_lens, const void* q, const void* k, const void* v,
                         void* o, float softmax_scale, unsigned flags,
@@ -542,13 +653,12 @@ int pgsr_full_reset_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_
   int rc = check_seqs(p, n, seqs);
   if (rc) return rc;
   // Validate the replay as it will run after the crop (prefix 0, rows emptied).
-  std::vector<int32_t> prefix(n), nalloc(n);
-  int32_t free_after = p->h_top;
+  std::vector<int32_t> prefix(n), nalloc(n), zeros(n, 0);
+  int32_t free_after = p->h_top + (layer == 0 ? (int32_t)count_freed(p, n, seqs, zeros.data()) : 0);
   for (int32_t i = 0; i < n; ++i) {
     if (layer == 0) {
       prefix[i] = 0;
       nalloc[i] = 0;
-      free_after += p->h_nalloc[seqs[i]];
     } else {
       prefix[i] = p->h_len[seqs[i]];
       nalloc[i] = p->h_nalloc[seqs[i]];
@@ -559,7 +669,6 @@ int pgsr_full_reset_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_
   if (rc) return rc;
   hipStream_t st = (hipStream_t)stream;
   if (layer == 0 && n > 0) {
-    std::vector<int32_t> zeros(n, 0);
     rc = do_crop(p, n, seqs, zeros.data(), 0, st);
     if (rc) return rc;
   }

@@ -48,6 +48,7 @@ class KVPool:
         self.seq_lens = torch.empty((max_seqs,), dtype=torch.int32, device=device)
         self.free_list = torch.empty((n_blocks,), dtype=torch.int32, device=device)
         self.free_top = torch.empty((1,), dtype=torch.int32, device=device)
+        self.ref_counts = torch.empty((n_blocks,), dtype=torch.int32, device=device)
         self.workspace = (torch.empty((workspace_bytes,), dtype=torch.uint8, device=device)
                           if workspace_bytes else None)
         order = N.int32_array(init_free_order) if init_free_order is not None else None
@@ -56,7 +57,7 @@ class KVPool:
             n_layers, n_q_heads, n_kv_heads, head_dim, block_size, dtype, n_blocks, max_seqs,
             max_blocks_per_seq, self.k_cache.data_ptr(), self.v_cache.data_ptr(),
             self.block_tables.data_ptr(), self.seq_lens.data_ptr(), self.free_list.data_ptr(),
-            self.free_top.data_ptr(),
+            self.free_top.data_ptr(), self.ref_counts.data_ptr(),
             self.workspace.data_ptr() if self.workspace is not None else None,
             workspace_bytes, order, _stream_ptr(stream), ctypes.byref(handle)))
         self._h = handle
@@ -104,6 +105,11 @@ class KVPool:
         return N.lib.pgsr_kv_crop(self._h, len(seqs), N.int32_array(seqs), N.int32_array(new_lens),
                                   N.POISON if poison else 0, _stream_ptr(stream))
 
+    def fork(self, srcs: Sequence[int], dsts: Sequence[int], stream=None) -> int:
+        """Copy-on-write fork of srcs[i] into the empty dsts[i]; returns the status."""
+        return N.lib.pgsr_kv_fork(self._h, len(srcs), N.int32_array(srcs), N.int32_array(dsts),
+                                  _stream_ptr(stream))
+
     def _prefill(self, fn, layer, seqs, q_lens, q, k, v, o, scale, commit, stream) -> int:
         dt = self.dtype
         return fn(self._h, layer, len(seqs), N.int32_array(seqs), N.int32_array(q_lens),
@@ -125,13 +131,17 @@ class KVPool:
     def state(self):
         torch.cuda.synchronize()
         return {"tables": self.block_tables.cpu().numpy(), "lens": self.seq_lens.cpu().numpy(),
-                "free": self.free_list.cpu().numpy(), "top": int(self.free_top.item())}
+                "free": self.free_list.cpu().numpy(), "top": int(self.free_top.item()),
+                "refs": self.ref_counts.cpu().numpy()}
+
+    def _meta(self):
+        return (self.block_tables, self.seq_lens, self.free_list, self.free_top, self.ref_counts)
 
     def save_meta(self):
-        return [t.clone() for t in (self.block_tables, self.seq_lens, self.free_list, self.free_top)]
+        return [t.clone() for t in self._meta()]
 
     def load_meta(self, saved) -> None:
-        for dst, src in zip((self.block_tables, self.seq_lens, self.free_list, self.free_top), saved):
+        for dst, src in zip(self._meta(), saved):
             dst.copy_(src)
         self.refresh()
 

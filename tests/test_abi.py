@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(native):
 
 
 def test_abi_version_and_workspace_size(native):
-    assert native.lib.pgsr_abi_version() == 1
+    assert native.lib.pgsr_abi_version() == 2
     assert native.lib.pgsr_workspace_bytes(32, 128, 2048, 4) == 2048 * 32 * 4 * 130 * 4
     assert native.lib.pgsr_workspace_bytes(32, 128, 2048, 1) == 0
 
@@ -51,7 +51,7 @@ def test_create_rejects_bad_geometry_before_any_device_call(native):
         a = {**args, **kw}
         return native.lib.pgsr_pool_create(a["n_layers"], a["hq"], a["hkv"], a["d"], a["B"], a["dt"],
                                            a["nb"], a["ms"], a["mbps"], fake, fake, fake, fake, fake,
-                                           fake, None, 0, None, None, ctypes.byref(out))
+                                           fake, fake, None, 0, None, None, ctypes.byref(out))
     assert create(d=96) == native.EUNSUPPORTED
     assert create(B=8) == native.EUNSUPPORTED
     assert create(hq=30) == native.EUNSUPPORTED
@@ -60,14 +60,19 @@ def test_create_rejects_bad_geometry_before_any_device_call(native):
     assert create(nb=0) == native.EINVAL
     order = native.int32_array([0, 1, 1] + list(range(3, 64)))
     assert native.lib.pgsr_pool_create(1, 32, 8, 128, 16, native.BF16, 64, 2, 8, fake, fake, fake,
-                                       fake, fake, fake, None, 0, order, None,
+                                       fake, fake, fake, fake, None, 0, order, None,
                                        ctypes.byref(out)) == native.EINVAL
     assert b"permutation" in native.lib.pgsr_last_error()
     assert not out.value
+    # a missing ref_counts array is rejected before any device call
+    assert native.lib.pgsr_pool_create(1, 32, 8, 128, 16, native.BF16, 64, 2, 8, fake, fake, fake,
+                                       fake, fake, fake, None, None, 0, None, None,
+                                       ctypes.byref(out)) == native.EINVAL
 
 
 def test_null_pool_and_gemm_validation(native):
     assert native.lib.pgsr_kv_crop(None, 0, None, None, 0, None) == native.EINVAL
+    assert native.lib.pgsr_kv_fork(None, 0, None, None, None) == native.EINVAL
     assert native.lib.pgsr_gemm_bf16(4, 12, 16, None, None, None, None, None) == native.EUNSUPPORTED
     assert native.lib.pgsr_gemm_bf16(0, 16, 16, None, None, None, None, None) == native.OK
     assert native.lib.pgsr_gemm_bf16(4, 16, 16, None, None, None, None, None) == native.EINVAL
