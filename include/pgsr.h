@@ -206,6 +206,33 @@ int pgsr_gemm_bf16(int32_t m, int32_t n, int32_t k, const void *x, const void *w
                    const void *r, void *y, void *stream);
 
 /*
+ * Elementwise steps of a full decoder layer around the projections (F of
+ * Eq. (1) at the real geometries; the layer itself follows the public
+ * architecture of the model families the paper runs).  bf16 device arrays,
+ * row-major, fp32 arithmetic, one round-to-nearest-even per stored value.
+ *
+ * RMSNorm: y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * gain, rows of d_model
+ * (a multiple of 8); y may alias x.
+ */
+int pgsr_rmsnorm_bf16(int32_t n, int32_t d_model, const void *x, const void *gain, float eps, void *y,
+                      void *stream);
+/*
+ * Rotary embedding in place on x [n][n_heads][head_dim] (head_dim even): for
+ * i < head_dim/2 the pair (x_i, x_{i + head_dim/2}) of token t turns by
+ * positions[t] * theta^(-2i/head_dim).  positions: device int32 [n], the
+ * tokens' absolute positions, so a replay from P rotates exactly as the full
+ * run does.  The angle is reduced in fp64.
+ */
+int pgsr_rope_bf16(int32_t n, int32_t n_heads, int32_t head_dim, void *x, const int32_t *positions,
+                   double theta, void *stream);
+/*
+ * SwiGLU gate: out[r][j] = SiLU(gate_up[r][j]) * gate_up[r][d_ff + j] with
+ * SiLU(g) = g / (1 + e^-g); gate_up [n][2 d_ff], out [n][d_ff], d_ff a
+ * multiple of 8.
+ */
+int pgsr_silu_mul_bf16(int32_t n, int32_t d_ff, const void *gate_up, void *out, void *stream);
+
+/*
  * Next-token sampling for the re-decode of model-derived suffix content
  * (Section 3.2, after Lemma 2), deterministic as Theorem 1's assumption A1
  * asks: the randomness source is fixed by (seed, stream, position).

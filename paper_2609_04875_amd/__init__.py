@@ -13,9 +13,10 @@ from ._native import (BF16, COMMIT, EHIP, EINVAL, ENOENT, ENOMEM, EUNSUPPORTED, 
                       POISON, PgsrError)
 from .frontend import CheckpointStore, ForgetPlan, ProvenanceGraph, forget_plan
 from .sampling import sample_tokens, sample_workspace_bytes
+from .decoder import DecoderReplay, rmsnorm, rope_, silu_mul
 from .pool import KVPool, gemm_bf16, workspace_bytes
 from .stack import StackedReplay
 
-__all__ = ["KVPool", "StackedReplay", "gemm_bf16", "workspace_bytes", "ProvenanceGraph", "CheckpointStore",
+__all__ = ["KVPool", "StackedReplay", "DecoderReplay", "rmsnorm", "rope_", "silu_mul", "gemm_bf16", "workspace_bytes", "ProvenanceGraph", "CheckpointStore",
            "ForgetPlan", "forget_plan", "sample_tokens", "sample_workspace_bytes", "PgsrError", "OK", "EINVAL", "ERANGE", "ENOMEM", "EUNSUPPORTED",
            "EHIP", "ENOENT", "F32", "BF16", "COMMIT", "POISON"]

@@ -27,7 +27,8 @@ EXPORTS = (
     "pgsr_graph_session_length", "pgsr_graph_kv_length_after", "pgsr_graph_locate_source",
     "pgsr_graph_taint_closure", "pgsr_graph_policy_boundaries", "pgsr_ckpt_create",
     "pgsr_ckpt_destroy", "pgsr_ckpt_register", "pgsr_ckpt_count", "pgsr_forget_plan_query",
-    "pgsr_sample_workspace_bytes", "pgsr_sample_tokens",
+    "pgsr_sample_workspace_bytes", "pgsr_sample_tokens", "pgsr_rmsnorm_bf16", "pgsr_rope_bf16",
+    "pgsr_silu_mul_bf16",
 )
 
 
@@ -93,6 +94,12 @@ def _load() -> ctypes.CDLL:
     lib.pgsr_sample_tokens.restype = ctypes.c_int
     lib.pgsr_sample_tokens.argtypes = [i32, i32, i32, P, f32, ctypes.c_uint64, P, P, P, ctypes.c_size_t,
                                        P, P]
+    lib.pgsr_rmsnorm_bf16.restype = ctypes.c_int
+    lib.pgsr_rmsnorm_bf16.argtypes = [i32, i32, P, P, f32, P, P]
+    lib.pgsr_rope_bf16.restype = ctypes.c_int
+    lib.pgsr_rope_bf16.argtypes = [i32, i32, i32, P, P, ctypes.c_double, P]
+    lib.pgsr_silu_mul_bf16.restype = ctypes.c_int
+    lib.pgsr_silu_mul_bf16.argtypes = [i32, i32, P, P, P]
     # forget front-end (host only)
     i64p = ctypes.POINTER(i64)
     for name, args in (

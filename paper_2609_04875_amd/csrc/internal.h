@@ -167,6 +167,12 @@ hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
                             int32_t* free_list, int32_t n_blocks, int32_t* free_top, int32_t* refs,
                             hipStream_t s);
+hipError_t launch_rmsnorm(int32_t n, int32_t dm, const void* x, const void* g, float eps, void* y,
+                          hipStream_t s);
+hipError_t launch_rope(int32_t n, int32_t heads, int32_t d, void* x, const int32_t* pos, double theta,
+                       hipStream_t s);
+hipError_t launch_silu_mul(int32_t n, int32_t dff, const void* gu, void* out, hipStream_t s);
+
 // Text returned by pgsr_last_error() on this thread (host runtime).
 void set_error(const char* msg);
 void clear_error();

@@ -733,4 +733,33 @@ int pgsr_sample_tokens(int32_t n, int32_t vocab, int32_t dtype, const void* logi
   return ok();
 }
 
+int pgsr_rmsnorm_bf16(int32_t n, int32_t d_model, const void* x, const void* gain, float eps, void* y,
+                      void* stream) {
+  if (n < 0 || d_model <= 0 || d_model % 8) return fail(PGSR_EINVAL, "n = %d, d_model = %d", n, d_model);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(PGSR_EINVAL, "eps must be finite and >= 0");
+  if (n == 0) return ok();
+  if (!x || !gain || !y) return fail(PGSR_EINVAL, "null pointer");
+  hipError_t err = launch_rmsnorm(n, d_model, x, gain, eps, y, (hipStream_t)stream);
+  return err == hipSuccess ? ok() : hip_fail(err, "rmsnorm launch");
+}
+
+int pgsr_rope_bf16(int32_t n, int32_t n_heads, int32_t head_dim, void* x, const int32_t* positions,
+                   double theta, void* stream) {
+  if (n < 0 || n_heads <= 0 || head_dim <= 0 || head_dim % 2)
+    return fail(PGSR_EINVAL, "n = %d, heads = %d, head_dim = %d", n, n_heads, head_dim);
+  if (!(theta > 1.0) || !std::isfinite(theta)) return fail(PGSR_EINVAL, "theta must be finite and > 1");
+  if (n == 0) return ok();
+  if (!x || !positions) return fail(PGSR_EINVAL, "null pointer");
+  hipError_t err = launch_rope(n, n_heads, head_dim, x, positions, theta, (hipStream_t)stream);
+  return err == hipSuccess ? ok() : hip_fail(err, "rope launch");
+}
+
+int pgsr_silu_mul_bf16(int32_t n, int32_t d_ff, const void* gate_up, void* out, void* stream) {
+  if (n < 0 || d_ff <= 0 || d_ff % 8) return fail(PGSR_EINVAL, "n = %d, d_ff = %d", n, d_ff);
+  if (n == 0) return ok();
+  if (!gate_up || !out) return fail(PGSR_EINVAL, "null pointer");
+  hipError_t err = launch_silu_mul(n, d_ff, gate_up, out, (hipStream_t)stream);
+  return err == hipSuccess ? ok() : hip_fail(err, "silu_mul launch");
+}
+
 }  // extern "C"
