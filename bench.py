@@ -7,7 +7,8 @@ workload is the 8B attention geometry: 32 query / 8 KV heads, d = 128, bf16, a
 contaminated cache of 10240 tokens cropped to 8189 (not a multiple of the
 16-token block) and a 2048-token suffix replayed against it.  ``--workload``
 selects the other workloads (tiny fp32 episode, 16 ragged episodes in one
-varlen launch, 32k-prefix chunked replay, the 8-layer stacked workload,
+varlen launch, 32k-prefix chunked replay, the 8-layer stacked workload, 4 full
+decoder layers at the 8B geometry (``llama8b_4layer_decoder_t8192_bf16``),
 ``decode``: one-token steps over 32 cached sequences with seeded sampling,
 and ``frontend``: the host-side forget queries that produce the crop length).  Inputs are seeded synthetic
 tensors resident in HBM before timing starts.
@@ -302,6 +303,106 @@ def copy_calibration(mib: int) -> None:
     torch.cuda.synchronize()
 
 
+def bench_decoder(args):
+    """Full decoder layers at the Llama-3.1-8B geometry (d_model 4096, 32/8
+    heads, d 128, d_ff 14336; RMSNorm, rotary embedding at absolute positions,
+    SwiGLU MLP), 4 layers, T = 8192 random-init tokens: crop + replay of the
+    suffix from tau - 1 = 50 % and 75 % of T through every layer, against the
+    full reset of all T tokens.  The roofline is the dominant kernel, the fused
+    gate/up projection (S x 28672 x 4096)."""
+    import torch
+    from paper_2609_04875_amd import DecoderReplay, gemm_bf16
+    L, dm, hq, hkv, d, dff, T, eps, theta = 4, 4096, 32, 8, 128, 14336, 8192, 1e-5, 5e5
+    g = torch.Generator(device="cuda").manual_seed(11)
+    rnd = lambda *shape, s=1.0: (torch.randn(*shape, device="cuda", generator=g) * s).to(torch.bfloat16)
+    ws = [{"wq": rnd(hq * d, dm, s=dm ** -0.5), "wk": rnd(hkv * d, dm, s=dm ** -0.5),
+           "wv": rnd(hkv * d, dm, s=dm ** -0.5), "wo": rnd(dm, hq * d, s=(hq * d) ** -0.5),
+           "w_gate_up": rnd(2 * dff, dm, s=dm ** -0.5), "w_down": rnd(dm, dff, s=dff ** -0.5),
+           "g_attn": (1 + rnd(dm, s=0.1).float()).to(torch.bfloat16),
+           "g_mlp": (1 + rnd(dm, s=0.1).float()).to(torch.bfloat16)} for _ in range(L)]
+    nbps = -(-T // 16)
+    dec = DecoderReplay(ws, hq, hkv, d, eps, theta, n_blocks=2 * nbps + 8, max_seqs=2,
+                        max_blocks_per_seq=nbps + 4)
+    pool = dec.pool
+    x0, xc = rnd(T, dm), rnd(T, dm)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, reps):
+        ms = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            ev[0].record()
+            fn()
+            ev[1].record()
+            torch.cuda.synchronize()
+            ms.append(ev[0].elapsed_time(ev[1]))
+        return ms
+
+    reps = max(1, args.steps // 4)
+    full_ms = timed(lambda: dec.full_reset(1, x0), reps)
+    flops_tok = 2.0 * dm * (hq + 2 * hkv) * d + 2.0 * hq * d * dm + 2.0 * dm * 3 * dff
+    points = []
+    for frac in (0.5, 0.75):
+        P = int(frac * T)
+        S = T - P
+        pool.crop([0], [0])
+        dec.replay(0, torch.cat([x0[:P], xc[P:]]))        # contaminated run into the cache
+        torch.cuda.synchronize()
+        saved = pool.save_meta()
+        xs = x0[P:].contiguous()
+
+        def step():
+            dec.crop([0], [P])
+            dec.replay(0, xs)
+        ms = []
+        for i in range(args.warmup + reps):
+            pool.load_meta(saved)
+            m = timed(step, 1)[0]
+            if i >= args.warmup:
+                ms.append(m)
+        fl = (flops_tok * S + attention_flops(P, S, hq, d)) * L
+        points.append({"prefix": P, "recomputed_tokens": S, "token_ratio": T / S,
+                       "replay_ms": float(np.mean(ms)), "full_reset_ms": float(np.mean(full_ms)),
+                       "wall_time_ratio": float(np.mean(full_ms) / np.mean(ms)),
+                       "replay_TFLOPs": fl / (np.mean(ms) * 1e-3) / 1e12})
+    S = T - points[0]["prefix"]
+    h = rnd(S, dm)
+    gu = torch.empty((S, 2 * dff), dtype=torch.bfloat16, device="cuda")
+    gemm_ms = float(np.median(timed(lambda: gemm_bf16(h, ws[0]["w_gate_up"], out=gu), 5)))
+    gflops = 2.0 * S * dm * 2 * dff
+    total_tokens = sum(p["recomputed_tokens"] for p in points)
+    total_ms = sum(p["replay_ms"] for p in points)
+    result = {
+        "metric": METRIC, "value": total_tokens / (total_ms * 1e-3), "unit": "tokens/s",
+        "n_gpus": 1, "steps": reps, "warmup": args.warmup, "ms_per_step": total_ms / len(points),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama8b_4layer_decoder_t8192_bf16", "t_total": T, "layers": L,
+                   "d_model": dm, "d_ff": dff, "n_q_heads": hq, "n_kv_heads": hkv, "head_dim": d,
+                   "prefix_fracs": [0.5, 0.75], "block_size": 16, "rope_theta": theta, "rms_eps": eps},
+        "roofline": {"bound": "mfma", "achieved": gflops / (gemm_ms * 1e-3) / 1e12,
+                     "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
+                     "frac": gflops / (gemm_ms * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"], "traffic": None,
+                     "kernel": "gemm_bf16_kernel (gate/up, S x 28672 x 4096)", "kernel_ms": gemm_ms},
+        "points": points,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import decoder as DEC
+        f64 = lambda t: t.float().cpu().numpy().astype(np.float64)
+        layers = [{"wq": f64(w["wq"]).T, "wk": f64(w["wk"]).T, "wv": f64(w["wv"]).T, "wo": f64(w["wo"]).T,
+                   "wg": f64(w["w_gate_up"][:dff]).T, "wu": f64(w["w_gate_up"][dff:]).T,
+                   "wd": f64(w["w_down"]).T, "g_attn": f64(w["g_attn"]), "g_mlp": f64(w["g_mlp"])} for w in ws]
+        n = 32
+        t0 = time.perf_counter()
+        DEC.decoder_layers(f64(x0[:n]), layers, hq, hkv, d, eps, theta)
+        dt = time.perf_counter() - t0
+        import oracle
+        result["cpu_baseline"] = {"value": n / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+                                  "sample": f"{n} tokens from position 0 through the 4 layers"}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def bench_decode(args):
     """Re-decode of model-derived suffix content (Section 3.2 after Lemma 2):
     32 sequences with 8192-token caches (8B geometry, bf16), one token per
@@ -468,6 +569,8 @@ def main() -> int:
         return bench_stack(args)
     if args.workload.startswith("decode"):
         return bench_decode(args)
+    if args.workload.startswith("llama8b_4layer_decoder"):
+        return bench_decoder(args)
     st = Setup(args.workload)
     w, g, pool = st.w, st.w.geometry, st.pool
     single_call = st.calls_per_step == 1
