@@ -1,18 +1,21 @@
 // fp32 prefix + causal prefill attention over the paged cache.
 //
-// One wave64 workgroup handles 64 consecutive query tokens of one query head;
-// each lane owns one query row.  Keys are visited in tiles of KT at absolute
-// positions 0, KT, 2KT, ... (the same tiling for any prefix length, so a row's
-// result depends only on its absolute position: a selective replay and a full
-// reset produce identical bits for the same query).  Each tile is gathered
-// through the block table into LDS; a lane computes its KT logits with FMAs,
-// masks keys past its position by select, and folds the tile into an online
-// softmax (running max m, running sum l, rescaled accumulator) in the base-2
-// domain.  Keys at or beyond the sequence length are never loaded: their LDS
-// rows are zero, so stale or NaN slots cannot leak into the result.
+// A workgroup of four waves handles 64 consecutive query tokens of one query
+// head; in every wave, lane i owns query row i.  Keys are visited in tiles of
+// KT at absolute positions 0, KT, 2KT, ...; wave w takes the tiles whose index
+// is w mod 4, each into its own LDS region (no workgroup barrier in the loop),
+// and keeps its own online softmax (running max m, running sum l, rescaled
+// accumulator, base-2 domain).  The four partial states are merged at the end
+// in the fixed order 0, 1, 2, 3.  Tile ownership depends only on absolute
+// positions, so a row's result depends only on its position and its keys: a
+// selective replay and a full reset produce identical bits.  Keys at or past
+// the sequence length are never loaded: their LDS rows are zero, so stale or
+// NaN slots cannot leak into the result.
 //
-// This path exists for fp32 accuracy (the fp32 tolerance is 1e-4 against fp64);
-// the bf16 MFMA kernel is the performance path.
+// Tiles are gathered with 16-byte loads; K rows and V rows sit in LDS
+// key-major without padding, read as 16-byte broadcasts (every lane reads the
+// same key).  This path exists for fp32 accuracy (1e-4 against fp64); the
+// bf16 MFMA kernel is the performance path.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -24,11 +27,14 @@ namespace pgsr {
 namespace {
 
 constexpr int kTokens = 64;  // query tokens per workgroup (one per lane)
+constexpr int kWaves = 4;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int D, int KT>
-__global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
-  __shared__ float ks[KT][D + 1];
-  __shared__ float vs[KT][D + 1];
+__global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
+  constexpr int KV = KT * D;                      // floats per tile operand
+  __shared__ __attribute__((aligned(16))) float lds[kWaves][2][KV];
 
   const int tile = blockIdx.x;
   const int hq = blockIdx.y;
@@ -39,23 +45,22 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
   const int G = a.n_q_heads / a.n_kv_heads;
   const int g = hq / G;
   const int B = a.block_size;
-  const int lane = threadIdx.x;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int t = lt * kTokens + lane;             // token index inside the suffix
   const bool valid = t < e.q_len;
   const int qpos = valid ? e.prefix + t : -1;    // absolute position (-1: padding row)
   const int t_last = min(e.q_len, (lt + 1) * kTokens) - 1;
   const int kv_len = e.prefix + e.q_len;
-  const int key_end = e.prefix + t_last + 1;     // keys this workgroup needs: [0, key_end)
+  const int n_kt = (e.prefix + t_last + 1 + KT - 1) / KT;   // tiles covering keys [0, key_end)
 
-  const float* q = (const float*)a.q;
   float qr[D];
-  if (valid) {
-    const float* qp = q + ((int64_t)(e.q_off + t) * a.n_q_heads + hq) * D;
+  {
+    const float* qp = (const float*)a.q + ((int64_t)(e.q_off + (valid ? t : 0)) * a.n_q_heads + hq) * D;
 #pragma unroll
-    for (int c = 0; c < D; ++c) qr[c] = qp[c];
-  } else {
-#pragma unroll
-    for (int c = 0; c < D; ++c) qr[c] = 0.f;
+    for (int c = 0; c < D; c += 4) {
+      const f32x4 v = valid ? *(const f32x4*)(qp + c) : f32x4{0, 0, 0, 0};
+      qr[c] = v[0]; qr[c + 1] = v[1]; qr[c + 2] = v[2]; qr[c + 3] = v[3];
+    }
   }
   float acc[D];
 #pragma unroll
@@ -67,38 +72,54 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
   const float* kc = (const float*)a.k_cache;
   const float* vc = (const float*)a.v_cache;
   const float c2 = a.scale_log2;
+  float* ks = lds[w][0];
+  float* vs = lds[w][1];
 
-  for (int kb = 0; kb < key_end; kb += KT) {
-    __syncthreads();
-    for (int i = lane; i < KT * D; i += 64) {  // K rows: contiguous D per slot
-      const int j = i / D, c = i % D;
+  for (int kt = w; kt < n_kt; kt += kWaves) {
+    const int kb = kt * KT;
+    // K: slot rows of D floats, 4 at a time
+    for (int i = lane; i < KV / 4; i += 64) {
+      const int j = i / (D / 4), c = (i % (D / 4)) * 4;
       const int pos = kb + j;
-      float val = 0.f;
+      f32x4 val = {0, 0, 0, 0};
       if (pos < kv_len) {
         const int32_t id = row[pos / B];
-        val = kc[((layer_off + (int64_t)id * a.n_kv_heads + g) * B + pos % B) * D + c];
+        val = *(const f32x4*)(kc + ((layer_off + (int64_t)id * a.n_kv_heads + g) * B + pos % B) * D + c);
       }
-      ks[j][c] = val;
+      *(f32x4*)(ks + j * D + c) = val;
     }
-    for (int i = lane; i < KT * D; i += 64) {  // V^T rows: contiguous B per d
-      const int c = i / KT, j = i % KT;
-      const int pos = kb + j;
-      float val = 0.f;
+    // V: stored [d][slot] per block; 4 consecutive slots of one d at a time
+    for (int i = lane; i < KV / 4; i += 64) {
+      const int c = i / (KT / 4), j = (i % (KT / 4)) * 4;
+      const int pos = kb + j;                    // 4 slots of one block (B % 4 == 0)
+      f32x4 val = {0, 0, 0, 0};
       if (pos < kv_len) {
         const int32_t id = row[pos / B];
-        val = vc[((layer_off + (int64_t)id * a.n_kv_heads + g) * D + c) * B + pos % B];
+        val = *(const f32x4*)(vc + ((layer_off + (int64_t)id * a.n_kv_heads + g) * D + c) * B + pos % B);
+#pragma unroll
+        for (int r = 1; r < 4; ++r)
+          if (pos + r >= kv_len) val[r] = 0.f;
       }
-      vs[j][c] = val;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vs[(j + r) * D + c] = val[r];
     }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     float s[KT];
     float tmax = -INFINITY;
 #pragma unroll
     for (int j = 0; j < KT; ++j) {
-      float dot = 0.f;
+      float d0 = 0.f, d1 = 0.f;
 #pragma unroll
-      for (int c = 0; c < D; ++c) dot = fmaf(qr[c], ks[j][c], dot);
-      s[j] = (kb + j <= qpos) ? dot * c2 : -INFINITY;
+      for (int c = 0; c < D; c += 4) {
+        const f32x4 kv = *(const f32x4*)(ks + j * D + c);
+        d0 = fmaf(qr[c], kv[0], d0);
+        d1 = fmaf(qr[c + 1], kv[1], d1);
+        d0 = fmaf(qr[c + 2], kv[2], d0);
+        d1 = fmaf(qr[c + 3], kv[3], d1);
+      }
+      s[j] = (kb + j <= qpos) ? (d0 + d1) * c2 : -INFINITY;
       tmax = fmaxf(tmax, s[j]);
     }
     const float m_new = fmaxf(m, tmax);
@@ -112,15 +133,52 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
       const float p = exp2f(s[j] - m_use);
       l += p;
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc[c] = fmaf(p, vs[j][c], acc[c]);
+      for (int c = 0; c < D; c += 4) {
+        const f32x4 vv = *(const f32x4*)(vs + j * D + c);
+        acc[c] = fmaf(p, vv[0], acc[c]);
+        acc[c + 1] = fmaf(p, vv[1], acc[c + 1]);
+        acc[c + 2] = fmaf(p, vv[2], acc[c + 2]);
+        acc[c + 3] = fmaf(p, vv[3], acc[c + 3]);
+      }
     }
     m = m_new;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // reads done before the next tile's writes
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  if (valid) {
+
+  // Merge the four partial states in order 0, 1, 2, 3 through LDS (the tile
+  // buffers are free now): wave w >= 1 publishes, wave 0 folds it in.
+  float* pub = &lds[0][0][0];                    // [64][D + 2]
+  static_assert(kWaves * 2 * KV >= 64 * (D + 2), "merge buffer");
+  for (int src = 1; src < kWaves; ++src) {
+    __syncthreads();
+    if (w == src) {
+      float* p = pub + lane * (D + 2);
+#pragma unroll
+      for (int c = 0; c < D; ++c) p[c] = acc[c];
+      p[D] = m;
+      p[D + 1] = l;
+    }
+    __syncthreads();
+    if (w == 0) {
+      const float* p = pub + lane * (D + 2);
+      const float mo = p[D], lo = p[D + 1];
+      const float mn = fmaxf(m, mo);
+      const float mu = (mn == -INFINITY) ? 0.f : mn;
+      const float a0 = exp2f(m - mu), a1 = exp2f(mo - mu);
+      l = l * a0 + lo * a1;
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc[c] = acc[c] * a0 + p[c] * a1;
+      m = mn;
+    }
+  }
+  if (w == 0 && valid) {
     float* op = (float*)a.o + ((int64_t)(e.q_off + t) * a.n_q_heads + hq) * D;
     const float inv = 1.f / l;
 #pragma unroll
-    for (int c = 0; c < D; ++c) op[c] = acc[c] * inv;
+    for (int c = 0; c < D; c += 4)
+      *(f32x4*)(op + c) = f32x4{acc[c] * inv, acc[c + 1] * inv, acc[c + 2] * inv, acc[c + 3] * inv};
   }
 }
 
@@ -132,9 +190,9 @@ hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
   dim3 grid(a.n_tiles, a.n_q_heads);
   if (a.head_dim == 64)
-    hipLaunchKernelGGL((attn_f32_kernel<64, 32>), grid, dim3(64), 0, s, a);
+    hipLaunchKernelGGL((attn_f32_kernel<64, 32>), grid, dim3(kWaves * 64), 0, s, a);
   else if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_f32_kernel<128, 16>), grid, dim3(64), 0, s, a);
+    hipLaunchKernelGGL((attn_f32_kernel<128, 16>), grid, dim3(kWaves * 64), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
