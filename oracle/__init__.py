@@ -15,6 +15,7 @@ Contents, each following the paper's definitions:
   ``pgsr_oracle.c``): the prefill form of F (Eq. (1)) over the suffix.
 * :func:`bf16_round` -- round-to-nearest-even to bfloat16, from the format's
   definition (8 significant bits).
+* :func:`e4m3_round` -- rounding to FP8 E4M3 for the FP8 KV pool (F1, F2).
 * :func:`stacked_layers` -- the stacked random-init layer F used by the 70B-like
   workload (a reading: the paper defines no layer).
 * :func:`recomputed_transitions`, :func:`replay_gain` -- Corollary 1.
@@ -39,6 +40,16 @@ Readings where the paper is silent (it never describes paging):
      len mod B slots of every layer into it, and puts it in the row (the old
      block's count drops by 1); this pop comes before the R4 pops.  Without
      forks every count is 0 or 1 and R3/R4 are unchanged.
+
+Readings of the FP8 KV cache variant (the paper stores the cache at model
+precision; the variant halves the bytes a decode step reads):
+  F1 E4M3 rounding is round-to-nearest, ties to even, saturating: magnitudes
+     past the largest finite value 448 store as +-448 (infinities too), NaN
+     stays NaN (:func:`e4m3_round`);
+  F2 each layer has one K scale and one V scale (positive, finite); a value x
+     (bf16 from the projection) is stored as the code e4m3(fp32(x / scale)),
+     with fp32 the correctly rounded quotient, and read back as code * scale;
+     attention runs on the read-back values.
 """
 from __future__ import annotations
 
@@ -139,6 +150,26 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
 # --------------------------------------------------------------------------- #
 # block table + free list                                                      #
 # --------------------------------------------------------------------------- #
+E4M3_MAX = 448.0
+
+
+def e4m3_round(x: np.ndarray) -> np.ndarray:
+    """Round to the FP8 format E4M3 (OCP "e4m3fn": 1 sign, 4 exponent bits with
+    bias 7, 3 mantissa bits, subnormal step 2^-9, largest finite 448, no
+    infinities), to nearest with ties to even, from the format's definition.
+    Reading F1 (FP8 KV cache): magnitudes past 448 saturate to 448 (infinities
+    too); NaN stays NaN."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(x), 2 * E4M3_MAX)     # anything this large saturates; keeps inf out
+    with np.errstate(divide="ignore", invalid="ignore"):
+        e = np.maximum(np.floor(np.log2(np.where(a > 0, a, 1.0))), -6.0)   # binade, subnormals at -6
+        q = np.exp2(e - 3.0)                                                  # 3 mantissa bits
+        r = np.rint(a / q) * q                                                # ties to even
+    r = np.where(a > 0, r, 0.0)
+    r = np.minimum(r, E4M3_MAX)
+    return np.where(np.isnan(x), np.nan, np.copysign(r, x))
+
+
 def _cdiv(a: int, b: int) -> int:
     return -(-a // b)
 
@@ -156,8 +187,11 @@ class PoolModel:
 
     def __init__(self, n_blocks: int, max_seqs: int, max_blocks: int, block_size: int,
                  init_free_order: Optional[Sequence[int]] = None,
-                 n_layers: int = 0, n_kv_heads: int = 0, head_dim: int = 0):
+                 n_layers: int = 0, n_kv_heads: int = 0, head_dim: int = 0, kv_fp8: bool = False):
         self.B = block_size
+        self.kv_fp8 = kv_fp8                 # store codes (F1, F2); scales per layer
+        self.k_scales = np.ones(max(n_layers, 1))
+        self.v_scales = np.ones(max(n_layers, 1))
         self.n_blocks = n_blocks
         self.tables = np.full((max_seqs, max_blocks), -1, np.int32)
         self.lens = np.zeros(max_seqs, np.int32)
@@ -284,17 +318,33 @@ class PoolModel:
         return int(self.tables[seq, pos // self.B]), pos % self.B
 
     # -- data (oracle's own layout) --
+    def set_kv_scales(self, k_scales: Sequence[float], v_scales: Sequence[float]) -> None:
+        """F2: one K and one V scale per layer (fp32 values)."""
+        self.k_scales = np.asarray(k_scales, dtype=np.float32).astype(np.float64)
+        self.v_scales = np.asarray(v_scales, dtype=np.float32).astype(np.float64)
+
+    def quantize(self, x: np.ndarray, scale: float) -> np.ndarray:
+        """F2: the code values (as fp64) stored for x, e4m3(fp32(x / scale))."""
+        q = np.asarray(x, dtype=np.float64).astype(np.float32) / np.float32(scale)   # fp32 quotient
+        return e4m3_round(q.astype(np.float64))
+
     def write(self, layer: int, seq: int, start: int, k: np.ndarray, v: np.ndarray) -> None:
+        if self.kv_fp8:
+            k = self.quantize(k, self.k_scales[layer])
+            v = self.quantize(v, self.v_scales[layer])
         for t in range(k.shape[0]):
             b, o = self.slot(seq, start + t)
             self.kdata[layer, b, o] = k[t]
             self.vdata[layer, b, o] = v[t]
 
     def gather(self, layer: int, seq: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
-        """Logical K, V of tokens 0 .. n-1 of ``seq`` read through the block table."""
+        """Logical K, V of tokens 0 .. n-1 of ``seq`` read through the block table
+        (FP8 pools: code * scale, F2)."""
         idx = [self.slot(seq, p) for p in range(n)]
         k = np.stack([self.kdata[layer, b, o] for b, o in idx]) if n else np.zeros((0,) + self.kdata.shape[3:])
         v = np.stack([self.vdata[layer, b, o] for b, o in idx]) if n else np.zeros((0,) + self.vdata.shape[3:])
+        if self.kv_fp8:
+            k, v = k * self.k_scales[layer], v * self.v_scales[layer]
         return k, v
 
     def state(self) -> Dict[str, np.ndarray]:
