@@ -38,8 +38,11 @@ Readings where the paper is silent (it never describes paging):
      would write into a partial tail block (len mod B != 0, S > 0) named by more
      than one entry first pops a private block, copies the tail block's first
      len mod B slots of every layer into it, and puts it in the row (the old
-     block's count drops by 1); this pop comes before the R4 pops.  Without
-     forks every count is 0 or 1 and R3/R4 are unchanged.
+     block's count drops by 1); this pop comes before the R4 pops.  The
+     sequences of one reservation are taken in call order, each seeing the
+     counts the earlier ones left (as in R3 and R4), so the last row still
+     naming a shared tail writes into it without a copy.  Without forks every
+     count is 0 or 1 and R3/R4 are unchanged.
 
 Readings of the FP8 KV cache variant (the paper stores the cache at model
 precision; the variant halves the bytes a decode step reads):
@@ -285,11 +288,21 @@ class PoolModel:
             if blocks > self.tables.shape[1]:
                 return ERANGE
             need.append(max(0, blocks - int(self.nalloc[s])))
-        cow = [self._shared_tail(s, S) for s, S in zip(seqs, q_lens)]
-        if sum(need) + sum(cow) > self.top:
+        # copies needed, in call order: each one releases an entry of its tail block (R5)
+        refs_left = {}
+        n_cow = 0
+        for s, S in zip(seqs, q_lens):
+            L = int(self.lens[s])
+            if S > 0 and L % self.B != 0:
+                b = int(self.tables[s, L // self.B])
+                r = refs_left.get(b, int(self.refs[b]))
+                if r > 1:
+                    n_cow += 1
+                    refs_left[b] = r - 1
+        if sum(need) + n_cow > self.top:
             return ENOMEM
-        for s, n, c in zip(seqs, need, cow):
-            if c:                                             # private copy of the tail block (R5)
+        for s, S, n in zip(seqs, q_lens, need):
+            if self._shared_tail(s, S):                       # private copy of the tail block (R5)
                 j = int(self.lens[s]) // self.B
                 old = int(self.tables[s, j])
                 self.top -= 1

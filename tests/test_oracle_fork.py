@@ -62,23 +62,24 @@ def test_random_fork_crop_append_isolation(seed):
     for _ in range(60):
         op = rng.integers(0, 3)
         s = int(rng.integers(0, n_seqs))
-        if op == 0:                                               # append S tokens on both layers
-            S = int(rng.integers(1, 2 * B + 3))
-            P = int(pool.lens[s])
-            if P + S > mb * B:
+        if op == 0:                        # append S_i tokens to 1-3 sequences in one call, both layers
+            seqs = rng.choice(n_seqs, size=int(rng.integers(1, 4)), replace=False).tolist()
+            sizes = [int(rng.integers(1, 2 * B + 3)) for _ in seqs]
+            if any(int(pool.lens[q]) + S > mb * B for q, S in zip(seqs, sizes)):
                 continue
             before = pool.state()
-            rc = pool.reserve([s], [S])
+            rc = pool.reserve(seqs, sizes)
             if rc != OK:
                 assert pool.state()["top"] == before["top"]
                 continue
-            vals = np.arange(stamp, stamp + S, dtype=np.float64)
-            stamp += S
-            for layer in range(2):
-                kv = (vals + 1000 * layer)[:, None, None]
-                pool.write(layer, s, P, kv, -kv)
-            pool.commit([s], [S])
-            shadow[s] += vals.tolist()
+            for q, S in zip(seqs, sizes):
+                vals = np.arange(stamp, stamp + S, dtype=np.float64)
+                stamp += S
+                for layer in range(2):
+                    kv = (vals + 1000 * layer)[:, None, None]
+                    pool.write(layer, q, int(pool.lens[q]), kv, -kv)
+                shadow[q] += vals.tolist()
+            pool.commit(seqs, sizes)
         elif op == 1:                                             # crop
             L = int(rng.integers(0, int(pool.lens[s]) + 1))
             assert pool.crop([s], [L]) == OK
@@ -110,3 +111,38 @@ def test_fork_errors_change_nothing():
         assert pool.fork(srcs, dsts) == EINVAL
         after = pool.state()
         assert all((after[k] == before[k]).all() for k in before)
+
+
+@pytest.mark.parametrize("r", [2, 3, 4])
+def test_one_reservation_by_every_sharer(r):
+    """r rows name one partial tail block; a reservation of all r in one call
+    makes r - 1 private copies and the last row in call order writes in place
+    (R5, call order), and it needs exactly r - 1 free blocks for them."""
+    B = 4
+    for order in ([0] + list(range(1, r)), list(range(r - 1, -1, -1))):
+        pool = PoolModel(2 + (r - 1), r, 4, B, n_layers=1, n_kv_heads=1, head_dim=1)
+        assert pool.reserve([0], [6]) == OK                   # blocks 0, 1; tail of 2 slots
+        pool.write(0, 0, 0, np.arange(6.0)[:, None, None], -np.arange(6.0)[:, None, None])
+        pool.commit([0], [6])
+        assert pool.fork([0] * (r - 1), list(range(1, r))) == OK
+        assert pool.top == r - 1 and pool.refs[1] == r
+        assert pool.reserve(order, [1] * r) == OK             # one token each, all into the shared tail
+        assert pool.top == 0
+        assert pool.tables[order[-1], 1] == 1                 # the last one kept the original
+        assert len({int(pool.tables[s, 1]) for s in range(r)}) == r
+        for i, s in enumerate(order):
+            pool.write(0, s, 6, np.array([[[100.0 + i]]]), np.array([[[-100.0 - i]]]))
+        pool.commit(order, [1] * r)
+        _invariants(pool)
+        for i, s in enumerate(order):
+            k, v = pool.gather(0, s, 7)
+            assert k[:, 0, 0].tolist() == [0, 1, 2, 3, 4, 5, 100 + i]
+    # one block short: all-or-nothing ENOMEM
+    pool = PoolModel(2 + (r - 2), r, 4, B)
+    assert pool.reserve([0], [6]) == OK
+    pool.commit([0], [6])
+    assert pool.fork([0] * (r - 1), list(range(1, r))) == OK
+    before = pool.state()
+    assert pool.reserve(list(range(r)), [1] * r) == oracle.ENOMEM
+    after = pool.state()
+    assert all((after[k] == before[k]).all() for k in before)
