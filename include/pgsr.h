@@ -20,7 +20,7 @@
  * top, updated at call time in enqueue order; one pool must not be used from
  * two host threads at once.
  *
- * Device layout (elements of the pool dtype, row-major):
+ * Device layout (elements of the pool dtype -- 4, 2 or 1 bytes -- row-major):
  *   k_cache      [n_layers][n_blocks][n_kv_heads][block_size][head_dim]
  *   v_cache      [n_layers][n_blocks][n_kv_heads][head_dim][block_size]
  *                (values are stored transposed inside each block: the
@@ -66,7 +66,10 @@ enum {
     PGSR_ENOENT = 6         /* front-end: the target never entered, or no checkpoint precedes tau */
 };
 
-enum { PGSR_F32 = 0, PGSR_BF16 = 1 };
+/* Pool dtypes.  PGSR_FP8_E4M3 stores K/V as 1-byte OCP E4M3 codes with
+ * per-layer scales (pgsr_pool_set_kv_scales); its q, k, v inputs and o
+ * outputs are bf16 and attention runs in bf16 on the widened codes. */
+enum { PGSR_F32 = 0, PGSR_BF16 = 1, PGSR_FP8_E4M3 = 2 };
 
 /* flags */
 #define PGSR_COMMIT 1u        /* replay: advance each sequence's length by its q_len */
@@ -89,10 +92,11 @@ int pgsr_abi_version(void);
  * NULL means n_blocks-1 .. 0, so pops yield 0, 1, 2, ....  The KV caches are
  * not touched.  workspace (device, nullable) is scratch for split-key partial
  * results, workspace_bytes long (see pgsr_workspace_bytes); NULL disables
- * key splitting.  Supported: dtype PGSR_F32 or PGSR_BF16, head_dim 64 or 128,
- * block_size 16, 32 or 64, n_q_heads a multiple of n_kv_heads (bf16: at
- * most 32 query heads per KV head, any such group, e.g. 7 for 28 / 4
- * heads).  Blocks.
+ * key splitting.  Supported: dtype PGSR_F32, PGSR_BF16 or PGSR_FP8_E4M3,
+ * head_dim 64 or 128, block_size 16, 32 or 64, n_q_heads a multiple of
+ * n_kv_heads (bf16 and fp8: at most 32 query heads per KV head, any such
+ * group, e.g. 7 for 28 / 4 heads).  An FP8 pool starts with every scale 1.
+ * Blocks.
  */
 int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                      int32_t block_size, int32_t dtype, int32_t n_blocks, int32_t max_seqs,
@@ -101,6 +105,20 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
                      int32_t *free_top, int32_t *ref_counts, void *workspace,
                      size_t workspace_bytes, const int32_t *init_free_order, void *stream,
                      pgsr_pool **out);
+
+/*
+ * FP8 KV cache (a storage variant of the cache that Algorithm 1 crops and
+ * appends to; the paper keeps the cache at model precision): k_scales and
+ * v_scales (HOST, n_layers positive normal floats each) become the layers'
+ * scales for later appends and reads.  An appended bf16 value x of layer l is
+ * stored as the E4M3 code of the correctly rounded fp32 quotient x / scale,
+ * rounded to nearest even, magnitudes past 448 saturating to 448, NaN kept
+ * NaN; attention reads code * scale.  Codes already in the cache keep the
+ * scale they were written with only if the scale does not change: set the
+ * scales before the first append.  PGSR_EINVAL for a non-FP8 pool or a bad
+ * scale (then nothing changes).  Host only, no device work.
+ */
+int pgsr_pool_set_kv_scales(pgsr_pool *pool, const float *k_scales, const float *v_scales);
 
 /* Release the host object; device memory is the caller's. NULL is a no-op. */
 int pgsr_pool_destroy(pgsr_pool *pool);
@@ -162,7 +180,9 @@ int pgsr_kv_fork(pgsr_pool *pool, int32_t n, const int32_t *srcs, const int32_t 
  *      head h (KV head h / (n_q_heads / n_kv_heads)), softmax attention over
  *      keys 0 .. p:  o = sum_j softmax_j(softmax_scale * q.k_j) v_j.
  * q, o : [sum S_i][n_q_heads][head_dim];  k, v : [sum S_i][n_kv_heads][head_dim],
- * device, pool dtype, packed in seqs order.  seqs, q_lens: HOST arrays.
+ * device, pool dtype (bf16 for an FP8 pool, whose k_j and v_j are the
+ * stored codes times the layer's scales), packed in seqs order.  seqs,
+ * q_lens: HOST arrays.
  * flags & PGSR_COMMIT adds S_i to each length (set it on the last layer of a
  * step) and sum S_i to *recomputed_tokens (HOST, nullable) -- the count of
  * Corollary 1.  Outputs are bitwise reproducible run to run and depend only on

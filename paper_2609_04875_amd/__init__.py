@@ -9,8 +9,8 @@ package only allocates device memory with torch and marshals arguments.  The
 forget front-end (provenance queries and checkpoint choice that yield the crop
 length) is host code in the same library.
 """
-from ._native import (BF16, COMMIT, EHIP, EINVAL, ENOENT, ENOMEM, EUNSUPPORTED, ERANGE, F32, OK,
-                      POISON, PgsrError)
+from ._native import (BF16, COMMIT, EHIP, EINVAL, ENOENT, ENOMEM, EUNSUPPORTED, ERANGE, F32, FP8_E4M3,
+                      OK, POISON, PgsrError)
 from .frontend import CheckpointStore, ForgetPlan, ProvenanceGraph, forget_plan
 from .sampling import sample_tokens, sample_workspace_bytes
 from .decoder import DecoderReplay, rmsnorm, rope_, silu_mul
@@ -19,4 +19,4 @@ from .stack import StackedReplay
 
 __all__ = ["KVPool", "StackedReplay", "DecoderReplay", "rmsnorm", "rope_", "silu_mul", "gemm_bf16", "workspace_bytes", "ProvenanceGraph", "CheckpointStore",
            "ForgetPlan", "forget_plan", "sample_tokens", "sample_workspace_bytes", "PgsrError", "OK", "EINVAL", "ERANGE", "ENOMEM", "EUNSUPPORTED",
-           "EHIP", "ENOENT", "F32", "BF16", "COMMIT", "POISON"]
+           "EHIP", "ENOENT", "F32", "BF16", "FP8_E4M3", "COMMIT", "POISON"]

@@ -41,12 +41,19 @@
 // the 32 rows one MFMA operand read touches over distinct bank groups and keeps
 // every operand address a base plus an immediate offset.
 //
+// FP8 cache (E4M3 codes): the tile loads fetch 8 bytes where the bf16 path
+// fetches 16, and the codes widen to bf16 exactly (every E4M3 value has at
+// most 4 significant bits) before the LDS store, so everything after the store
+// is the bf16 kernel.  The K scale rides in the softmax scale, the V scale in
+// the output normalisation.
+//
 // Key tiles sit at absolute positions and rows never interact, so a query's
 // output bits depend only on its absolute position and its own keys: selective
 // replay and full reset agree bitwise, and repeated runs are bitwise identical.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -95,6 +102,20 @@ __device__ inline u32x4 zero_tail(u32x4 v, int pos0, int limit) {
   return v;
 }
 
+// Eight E4M3 codes (byte e = element e) as eight bf16 values, exactly: the
+// hardware conversion gives fp32 pairs, whose upper halves are the bf16 bits.
+__device__ inline u32x4 widen_fp8(u32x2 w) {
+  u32x4 r;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[h], false);   // bytes 0, 1
+    const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[h], true);    // bytes 2, 3
+    r[2 * h] = __builtin_amdgcn_perm(__float_as_uint(lo[1]), __float_as_uint(lo[0]), 0x07060302u);
+    r[2 * h + 1] = __builtin_amdgcn_perm(__float_as_uint(hi[1]), __float_as_uint(hi[0]), 0x07060302u);
+  }
+  return r;
+}
+
 // Block ids of one key tile (up to four blocks), indexed with a wave-uniform
 // value through selects rather than as an array, which would live in memory.
 struct Ids {
@@ -102,11 +123,13 @@ struct Ids {
   __device__ int32_t get(int i) const { return i == 0 ? v0 : i == 1 ? v1 : i == 2 ? v2 : v3; }
 };
 
-template <int D, int NW, int B>
+template <int D, int NW, int B, bool F8>
 __global__ void __launch_bounds__(NW * 64, 2)
 attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t* __restrict__ qg_,
-                 const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+                 const std::conditional_t<F8, uint8_t, uint16_t>* __restrict__ kc,
+                 const std::conditional_t<F8, uint8_t, uint16_t>* __restrict__ vc,
                  uint16_t* __restrict__ og) {
+  using Raw = std::conditional_t<F8, u32x2, u32x4>;   // 8 cache elements
   constexpr int KT = kKT;
   constexpr int KB = KT / B;               // blocks per key tile
   constexpr int KLD = D + 8;               // LDS row stride of the K tile (elements)
@@ -200,24 +223,28 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
     return ids;
   };
 
-  u32x4 kreg[CPT], vreg[CPT];
+  Raw kreg[CPT], vreg[CPT];
   auto load_tile = [&](const Ids& ids) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int in = chunk_in(i);
       const int64_t base = (head_base + (int64_t)ids.get(chunk_blk(i)) * hkv) * (B * D);
-      kreg[i] = *(const u32x4*)(kc + base + (in / (D / 8)) * D + (in % (D / 8)) * 8);
-      vreg[i] = *(const u32x4*)(vc + base + (in / (B / 8)) * B + (in % (B / 8)) * 8);
+      kreg[i] = *(const Raw*)(kc + base + (in / (D / 8)) * D + (in % (D / 8)) * 8);
+      vreg[i] = *(const Raw*)(vc + base + (in / (B / 8)) * B + (in % (B / 8)) * 8);
     }
+  };
+  auto as_bf16 = [](const Raw& x) {
+    if constexpr (F8) return widen_fp8(x);
+    else return x;
   };
   auto store_tile = [&](int buf, int kb) {
     const bool tail = kb + KT > kv_len;   // V slots at or past kv_len must read as 0
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int blk = chunk_blk(i), in = chunk_in(i);
-      *(u32x4*)&k_lds[buf][(blk * B + in / (D / 8)) * KLD + (in % (D / 8)) * 8] = kreg[i];
+      *(u32x4*)&k_lds[buf][(blk * B + in / (D / 8)) * KLD + (in % (D / 8)) * 8] = as_bf16(kreg[i]);
       const int dd = in / (B / 8), key0 = blk * B + (in % (B / 8)) * 8;
-      u32x4 val = vreg[i];
+      u32x4 val = as_bf16(vreg[i]);
       if (tail) {
         const int pos0 = kb + key0;
         if (pos0 >= kv_len) val = u32x4{0, 0, 0, 0};
@@ -371,7 +398,7 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
                   oacc[db][4 * i4 + 3]};
     if (hh == 0) *(f32x2*)(a.ws_ml + 2 * prow) = f32x2{m, l_tot};
   } else if (valid) {
-    const float inv = 1.f / l_tot;
+    const float inv = a.o_scale / l_tot;
     uint16_t* op = og + ((int64_t)(e.q_off + tok) * a.n_q_heads + hq) * D + 4 * hh;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -441,7 +468,7 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t
       o1 += wgt * a1[j];
     }
   }
-  const float inv = 1.f / L;
+  const float inv = a.o_scale / L;
   bf16x8 out;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -455,20 +482,21 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t
 
 int attn_bf16_tile_tokens(int, int group) { return kNW * (32 / group); }
 
-template <int D, int B>
+template <int D, int B, bool F8>
 static void launch_d_b(const AttnArgs& a, hipStream_t s) {
+  using CT = std::conditional_t<F8, uint8_t, uint16_t>;
   dim3 grid(a.n_tiles * a.n_kv_heads * a.n_splits);
-  hipLaunchKernelGGL((attn_bf16_kernel<D, kNW, B>), grid, dim3(kNW * 64), 0, s, a, a.tables,
-                     (const uint16_t*)a.q, (const uint16_t*)a.k_cache,
-                     (const uint16_t*)a.v_cache, (uint16_t*)a.o);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, kNW, B, F8>), grid, dim3(kNW * 64), 0, s, a, a.tables,
+                     (const uint16_t*)a.q, (const CT*)a.k_cache, (const CT*)a.v_cache,
+                     (uint16_t*)a.o);
 }
 
-template <int D>
+template <int D, bool F8>
 static hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
   switch (a.block_size) {
-    case 16: launch_d_b<D, 16>(a, s); break;
-    case 32: launch_d_b<D, 32>(a, s); break;
-    case 64: launch_d_b<D, 64>(a, s); break;
+    case 16: launch_d_b<D, 16, F8>(a, s); break;
+    case 32: launch_d_b<D, 32, F8>(a, s); break;
+    case 64: launch_d_b<D, 64, F8>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -489,8 +517,15 @@ hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
-  if (a.head_dim == 128) return launch_d<128>(a, s);
-  if (a.head_dim == 64) return launch_d<64>(a, s);
+  if (a.head_dim == 128) return launch_d<128, false>(a, s);
+  if (a.head_dim == 64) return launch_d<64, false>(a, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s) {
+  if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
+  if (a.head_dim == 128) return launch_d<128, true>(a, s);
+  if (a.head_dim == 64) return launch_d<64, true>(a, s);
   return hipErrorInvalidValue;
 }
 

@@ -94,6 +94,9 @@ struct AppendArgs {
   int32_t* refs;
   int32_t max_bps, n_blocks, n_kv_heads, block_size, head_dim, layer, n_layers;
   int32_t commit;
+  // FP8 E4M3 cache (1-byte elements) fed from bf16 inputs: each value is stored
+  // as the code of fp32(x / scale), rounded to nearest even, saturating at 448.
+  float k_scale, v_scale;
   int32_t write_top;   // 1: this launch writes free_top = top_after
   int32_t top_after;
   int32_t n;
@@ -117,7 +120,8 @@ struct AttnArgs {
   const void* v_cache;
   const int32_t* tables;
   int32_t max_bps, n_blocks, n_q_heads, n_kv_heads, block_size, head_dim, layer;
-  float scale_log2;    // softmax_scale * log2(e)
+  float scale_log2;    // softmax_scale * log2(e) (times the K scale of an FP8 cache)
+  float o_scale;       // output factor: the V scale of an FP8 cache, else 1
   int32_t n;
   int32_t n_tiles;
   // Split-key mode (n_splits > 1): split s of a query tile covers keys
@@ -162,6 +166,9 @@ hipError_t launch_fork(const ForkArgs& a, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
+// Same kernel over an FP8 E4M3 cache: codes widen to bf16 exactly on the way
+// into LDS; the K scale is in scale_log2, the V scale in o_scale.
+hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s);
 // Merge split-key partials into O (bf16), splits in increasing order.
 hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,

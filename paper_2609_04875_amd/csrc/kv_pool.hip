@@ -5,8 +5,9 @@
 // crop pushes a block only when its count reaches 0, and an append that would
 // write into a shared partial tail block first copies it into a private one.
 //
-// All of this is integer bookkeeping and bit copies: results are exact and do
-// not depend on the launch shape.  Work per call is tiny (a crop touches at
+// All of this is integer bookkeeping and bit copies (an FP8 cache adds a
+// rounding to E4M3 defined bit for bit): results are exact and do not depend
+// on the launch shape.  Work per call is tiny (a crop touches at
 // most a few KB of int32), so these kernels are launch-latency bound; they are
 // written for clarity and coalescing, not occupancy.
 #include <hip/hip_runtime.h>
@@ -153,6 +154,37 @@ __global__ void __launch_bounds__(256) cow_kernel(AppendArgs a) {
   }
 }
 
+// FP8 E4M3 code of x (OCP "e4m3fn": bias 7, 3 mantissa bits, largest finite
+// 448, NaN = 0x7F), round to nearest even, magnitudes from 464 on saturating
+// to 448 (464 itself is the tie between 448 and the next step, 480, which the
+// format lacks; ties go to the even mantissa 448 anyway).  Written from the
+// format's definition on the fp32 bits.
+__device__ inline uint8_t e4m3_code(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t sign = (u >> 24) & 0x80u;
+  const float a = fabsf(x);
+  if (!(a == a)) return (uint8_t)(sign | 0x7Fu);
+  if (a >= 464.f) return (uint8_t)(sign | 0x7Eu);
+  if (a < 0.015625f)                               // below 2^-6: subnormal steps of 2^-9
+    return (uint8_t)(sign | (uint32_t)__builtin_rintf(a * 512.f));   // exact product; 8 is 2^-6
+  const uint32_t au = u & 0x7FFFFFFFu;
+  uint32_t code = (((au >> 23) - 120u) << 3) | ((au >> 20) & 7u);   // exponent rebiased 127 -> 7
+  const uint32_t rest = au & 0xFFFFFu;                               // the 20 dropped mantissa bits
+  if (rest > 0x80000u || (rest == 0x80000u && (code & 1u))) ++code;  // a carry moves up a binade
+  return (uint8_t)(sign | code);
+}
+
+// Cache element for input element x: a bit copy, or (bf16 -> FP8) the code of
+// the correctly rounded fp32 quotient x / scale.
+template <typename TI, typename TC>
+__device__ inline TC to_cache(TI x, float) {
+  return x;
+}
+template <>
+__device__ inline uint8_t to_cache<uint16_t, uint8_t>(uint16_t x, float scale) {
+  return e4m3_code(__uint_as_float((uint32_t)x << 16) / scale);
+}
+
 // Reserve + append.  blockIdx.x enumerates (sequence, logical block) items,
 // blockIdx.y the KV head.  The physical id of a newly reserved logical block
 // lb is read straight from the stack (free_list[stack_before - 1 - k] for the
@@ -160,7 +192,7 @@ __global__ void __launch_bounds__(256) cow_kernel(AppendArgs a) {
 // write; the kv-head-0 workgroup records it in the table.
 //   K: token p -> k_cache[layer][id][h][p % B][:]      (row copy)
 //   V: token p -> v_cache[layer][id][h][:][p % B]      (transposed via LDS)
-template <typename T>
+template <typename TI, typename T>
 __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
   __shared__ T vstage[64 * 128];  // [slot][d], block_size <= 64, head_dim <= 128
   const int item = blockIdx.x;
@@ -190,15 +222,15 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
   const int nt = p1 - p0;  // tokens landing in this block (>= 1)
   const int s0 = p0 - lb * B;
   const int64_t blk = ((int64_t)a.layer * a.n_blocks + id) * a.n_kv_heads + h;
-  const T* kin = (const T*)a.k_in;
-  const T* vin = (const T*)a.v_in;
+  const TI* kin = (const TI*)a.k_in;
+  const TI* vin = (const TI*)a.v_in;
   T* kc = (T*)a.k_cache + blk * B * D;
   T* vc = (T*)a.v_cache + blk * D * B;
   for (int i = threadIdx.x; i < nt * D; i += blockDim.x) {
     const int t = i / D, c = i % D;
     const int64_t src = ((int64_t)(e.q_off + (p0 - e.prefix) + t) * a.n_kv_heads + h) * D + c;
-    kc[(int64_t)(s0 + t) * D + c] = kin[src];
-    vstage[t * D + c] = vin[src];
+    kc[(int64_t)(s0 + t) * D + c] = to_cache<TI, T>(kin[src], a.k_scale);
+    vstage[t * D + c] = to_cache<TI, T>(vin[src], a.v_scale);
   }
   __syncthreads();
   for (int i = threadIdx.x; i < nt * D; i += blockDim.x) {
@@ -239,8 +271,10 @@ hipError_t launch_poison(const PoisonArgs& a, hipStream_t s) {
   const dim3 grid(a.n_freed + a.n, a.n_layers);
   if (a.elem_bytes == 4)
     hipLaunchKernelGGL(poison_kernel<uint32_t>, grid, dim3(256), 0, s, a, (uint32_t)0x7FC00000u);
-  else
+  else if (a.elem_bytes == 2)
     hipLaunchKernelGGL(poison_kernel<uint16_t>, grid, dim3(256), 0, s, a, (uint16_t)0x7FC0u);
+  else
+    hipLaunchKernelGGL(poison_kernel<uint8_t>, grid, dim3(256), 0, s, a, (uint8_t)0x7Fu);
   return hipGetLastError();
 }
 
@@ -248,17 +282,17 @@ hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s) {
   if (a.n <= 0 || a.n_items <= 0) return hipSuccess;
   bool any_cow = false;
   for (int i = 0; i < a.n; ++i) any_cow |= a.e[i].cow_old >= 0;
-  if (any_cow) {
-    if (elem_bytes == 4)
-      hipLaunchKernelGGL(cow_kernel<uint32_t>, dim3(a.n, a.n_kv_heads), dim3(256), 0, s, a);
-    else
-      hipLaunchKernelGGL(cow_kernel<uint16_t>, dim3(a.n, a.n_kv_heads), dim3(256), 0, s, a);
+  const dim3 cow_grid(a.n, a.n_kv_heads), grid(a.n_items, a.n_kv_heads);
+  if (elem_bytes == 4) {
+    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint32_t>, cow_grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((append_kernel<uint32_t, uint32_t>), grid, dim3(256), 0, s, a);
+  } else if (elem_bytes == 2) {
+    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint16_t>, cow_grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((append_kernel<uint16_t, uint16_t>), grid, dim3(256), 0, s, a);
+  } else {                                          // FP8 cache, bf16 inputs
+    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint8_t>, cow_grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((append_kernel<uint16_t, uint8_t>), grid, dim3(256), 0, s, a);
   }
-  dim3 grid(a.n_items, a.n_kv_heads);
-  if (elem_bytes == 4)
-    hipLaunchKernelGGL(append_kernel<uint32_t>, grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(append_kernel<uint16_t>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -12,7 +12,9 @@
 #include <cstdio>
 #include <cstring>
 #include <numeric>
+#include <cfloat>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "internal.h"
@@ -39,6 +41,8 @@ struct pgsr_pool {
   int32_t h_top;
   // optional kernel timing: events around the append and attention launches
   bool timing = false, timed_call = false;
+  // FP8 pools: per-layer K and V scales (stored code = x / scale, read = code * scale)
+  std::vector<float> k_scale, v_scale;
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
 };
 
@@ -67,7 +71,7 @@ int hip_fail(hipError_t e, const char* what) {
 
 inline int32_t cdiv(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
-int elem_bytes(const pgsr_pool* p) { return p->dtype == PGSR_F32 ? 4 : 2; }
+int elem_bytes(const pgsr_pool* p) { return p->dtype == PGSR_F32 ? 4 : p->dtype == PGSR_BF16 ? 2 : 1; }
 
 // Distinct, in-range sequence ids.
 int check_seqs(const pgsr_pool* p, int32_t n, const int32_t* seqs) {
@@ -195,6 +199,9 @@ int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* se
     return fail(PGSR_EINVAL, "layer %d outside [0, %d)", layer, p->n_layers);
   if (!std::isfinite(scale)) return fail(PGSR_EINVAL, "softmax_scale is not finite");
   int64_t total = 0, need = 0;
+  // Private tail copies are decided in call order: each copy releases one
+  // entry of the shared block, so the last row naming it writes in place.
+  std::unordered_map<int32_t, int32_t> released;
   for (int32_t i = 0; i < n; ++i) {
     const int32_t S = q_lens[i];
     if (S < 0) return fail(PGSR_EINVAL, "q_lens[%d] = %d is negative", i, S);
@@ -203,7 +210,13 @@ int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* se
       return fail(PGSR_ERANGE, "sequence %d would reach %lld tokens; its row holds %lld",
                   seqs[i], (long long)end, (long long)p->max_bps * p->B);
     need += std::max<int64_t>(0, cdiv(end, p->B) - nalloc[i]);
-    if (nalloc[i] > 0 && shared_tail(p, seqs[i], prefix[i], S)) ++need;   // private tail copy
+    if (nalloc[i] > 0 && S > 0 && prefix[i] % p->B != 0) {
+      const int32_t b = p->h_tab[(size_t)seqs[i] * p->max_bps + prefix[i] / p->B];
+      if (b >= 0 && p->h_ref[b] - released[b] > 1) {   // private tail copy
+        ++need;
+        ++released[b];
+      }
+    }
     total += S;
   }
   if (total > INT32_MAX) return fail(PGSR_ERANGE, "more than 2^31-1 query tokens in one call");
@@ -255,6 +268,8 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.layer = layer;
     a.n_layers = p->n_layers;
     a.commit = commit ? 1 : 0;
+    a.k_scale = p->k_scale[layer];
+    a.v_scale = p->v_scale[layer];
     a.n = cnt;
     int32_t items = 0;
     for (int32_t i = 0; i < cnt; ++i) {
@@ -323,7 +338,8 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.block_size = p->B;
     a.head_dim = p->d;
     a.layer = layer;
-    a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634 * (double)p->k_scale[layer]);
+    a.o_scale = p->v_scale[layer];
     a.n = cnt;
     int32_t tiles = 0;
     for (int32_t i = 0; i < cnt; ++i) {
@@ -341,7 +357,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     // Split-key mode when the launch would leave CUs idle and the caller gave
     // a workspace for the partials: splits at absolute multiples of split_len.
     const int64_t wgs = (int64_t)tiles * p->hkv;
-    if (p->dtype == PGSR_BF16 && p->workspace && wgs < kSplitTargetWorkgroups) {
+    if (p->dtype != PGSR_F32 && p->workspace && wgs < kSplitTargetWorkgroups) {
       int32_t max_key = 0;
       for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);
       const int64_t per_split = (int64_t)a.n_rows * ((int64_t)p->d + 2) * (int64_t)sizeof(float);
@@ -355,7 +371,9 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
     }
-    hipError_t err = p->dtype == PGSR_F32 ? launch_attn_f32(a, st) : launch_attn_bf16(a, st);
+    hipError_t err = p->dtype == PGSR_F32    ? launch_attn_f32(a, st)
+                     : p->dtype == PGSR_BF16 ? launch_attn_bf16(a, st)
+                                             : launch_attn_fp8(a, st);
     if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine_bf16(a, st);
     if (err != hipSuccess) return hip_fail(err, "attention launch");
   }
@@ -405,14 +423,15 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
   if (n_q_heads % n_kv_heads != 0)
     return fail(PGSR_EUNSUPPORTED, "n_q_heads %d is not a multiple of n_kv_heads %d", n_q_heads,
                 n_kv_heads);
-  if (dtype != PGSR_F32 && dtype != PGSR_BF16) return fail(PGSR_EUNSUPPORTED, "dtype %d", dtype);
+  if (dtype != PGSR_F32 && dtype != PGSR_BF16 && dtype != PGSR_FP8_E4M3)
+    return fail(PGSR_EUNSUPPORTED, "dtype %d", dtype);
   if (head_dim != 64 && head_dim != 128)
     return fail(PGSR_EUNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
   if (block_size != 16 && block_size != 32 && block_size != 64)
     return fail(PGSR_EUNSUPPORTED, "block_size %d (supported: 16, 32, 64)", block_size);
   const int group = n_q_heads / n_kv_heads;
-  if (dtype == PGSR_BF16 && group > 32)
-    return fail(PGSR_EUNSUPPORTED, "bf16 kernels need n_q_heads / n_kv_heads <= 32");
+  if (dtype != PGSR_F32 && group > 32)
+    return fail(PGSR_EUNSUPPORTED, "bf16 and fp8 kernels need n_q_heads / n_kv_heads <= 32");
   if ((int64_t)max_seqs * max_blocks_per_seq > INT32_MAX)
     return fail(PGSR_ERANGE, "block table larger than 2^31-1 entries");
   if (!k_cache || !v_cache || !block_tables || !seq_lens || !free_list || !free_top || !ref_counts)
@@ -456,6 +475,8 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
   p->free_list = free_list;
   p->free_top = free_top;
   p->refs = ref_counts;
+  p->k_scale.assign(n_layers, 1.f);
+  p->v_scale.assign(n_layers, 1.f);
   p->workspace = workspace;
   p->workspace_bytes = workspace_bytes;
   p->h_len.assign(max_seqs, 0);
@@ -475,6 +496,18 @@ int pgsr_pool_destroy(pgsr_pool* pool) {
     for (hipEvent_t& e : pool->ev)
       if (e) (void)hipEventDestroy(e);
   delete pool;
+  return ok();
+}
+
+int pgsr_pool_set_kv_scales(pgsr_pool* p, const float* k_scales, const float* v_scales) {
+  if (!p || !k_scales || !v_scales) return fail(PGSR_EINVAL, "null argument");
+  if (p->dtype != PGSR_FP8_E4M3) return fail(PGSR_EINVAL, "KV scales apply to an FP8 pool only");
+  for (int32_t l = 0; l < p->n_layers; ++l)
+    for (const float x : {k_scales[l], v_scales[l]})
+      if (!(x >= FLT_MIN && x <= FLT_MAX))
+        return fail(PGSR_EINVAL, "scale of layer %d is not a positive normal float", l);
+  p->k_scale.assign(k_scales, k_scales + p->n_layers);
+  p->v_scale.assign(v_scales, v_scales + p->n_layers);
   return ok();
 }
 

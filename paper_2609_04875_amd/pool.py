@@ -14,7 +14,10 @@ import torch
 
 from . import _native as N
 
-_DT = {N.F32: torch.float32, N.BF16: torch.bfloat16}
+# (cache storage dtype, dtype of q / k / v / o) per pool dtype; an FP8 pool
+# holds raw E4M3 codes as bytes.
+_DT = {N.F32: (torch.float32, torch.float32), N.BF16: (torch.bfloat16, torch.bfloat16),
+       N.FP8_E4M3: (torch.uint8, torch.bfloat16)}
 
 
 def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> Optional[int]:
@@ -39,11 +42,11 @@ class KVPool:
         self.n_layers, self.hq, self.hkv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         self.n_blocks, self.max_seqs, self.max_bps = n_blocks, max_seqs, max_blocks_per_seq
         self.B, self.dtype_code = block_size, dtype
-        self.dtype = _DT[dtype]
+        self.cache_dtype, self.dtype = _DT[dtype]
         shape = (n_layers, n_blocks, n_kv_heads, block_size, head_dim)
-        self.k_cache = torch.zeros(shape, dtype=self.dtype, device=device)
+        self.k_cache = torch.zeros(shape, dtype=self.cache_dtype, device=device)
         self.v_cache = torch.zeros((n_layers, n_blocks, n_kv_heads, head_dim, block_size),
-                                   dtype=self.dtype, device=device)
+                                   dtype=self.cache_dtype, device=device)
         self.block_tables = torch.empty((max_seqs, max_blocks_per_seq), dtype=torch.int32, device=device)
         self.seq_lens = torch.empty((max_seqs,), dtype=torch.int32, device=device)
         self.free_list = torch.empty((n_blocks,), dtype=torch.int32, device=device)
@@ -87,6 +90,14 @@ class KVPool:
 
     def refresh(self, stream=None) -> None:
         N.check(N.lib.pgsr_pool_refresh(self._h, _stream_ptr(stream)))
+
+    def set_kv_scales(self, k_scales: Sequence[float], v_scales: Sequence[float]) -> None:
+        """Per-layer K and V scales of an FP8 pool (stored code = x / scale)."""
+        if len(k_scales) != self.n_layers or len(v_scales) != self.n_layers:
+            raise ValueError("one K and one V scale per layer")
+        ks = (ctypes.c_float * self.n_layers)(*map(float, k_scales))
+        vs = (ctypes.c_float * self.n_layers)(*map(float, v_scales))
+        N.check(N.lib.pgsr_pool_set_kv_scales(self._h, ks, vs))
 
     # ---- kernel timing (HIP events recorded by the library on the call's stream) ----
     def enable_timing(self, on: bool = True) -> None:

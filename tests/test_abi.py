@@ -57,6 +57,7 @@ def test_create_rejects_bad_geometry_before_any_device_call(native):
     assert create(hq=30) == native.EUNSUPPORTED
     assert create(hq=33, hkv=1) == native.EUNSUPPORTED       # bf16: at most 32 query heads per KV head
     assert create(dt=7) == native.EUNSUPPORTED
+    assert create(dt=native.FP8_E4M3, hq=33, hkv=1) == native.EUNSUPPORTED   # fp8 runs the bf16 kernel
     assert create(nb=0) == native.EINVAL
     order = native.int32_array([0, 1, 1] + list(range(3, 64)))
     assert native.lib.pgsr_pool_create(1, 32, 8, 128, 16, native.BF16, 64, 2, 8, fake, fake, fake,
@@ -73,6 +74,8 @@ def test_create_rejects_bad_geometry_before_any_device_call(native):
 def test_null_pool_and_gemm_validation(native):
     assert native.lib.pgsr_kv_crop(None, 0, None, None, 0, None) == native.EINVAL
     assert native.lib.pgsr_kv_fork(None, 0, None, None, None) == native.EINVAL
+    one = (ctypes.c_float * 1)(1.0)
+    assert native.lib.pgsr_pool_set_kv_scales(None, one, one) == native.EINVAL
     assert native.lib.pgsr_gemm_bf16(4, 12, 16, None, None, None, None, None) == native.EUNSUPPORTED
     assert native.lib.pgsr_gemm_bf16(0, 16, 16, None, None, None, None, None) == native.OK
     assert native.lib.pgsr_gemm_bf16(4, 16, 16, None, None, None, None, None) == native.EINVAL

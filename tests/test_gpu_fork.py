@@ -36,25 +36,30 @@ def test_random_fork_crop_append_match_oracle(seed):
     for step in range(40):
         op = int(rng.integers(0, 3))
         s = int(rng.integers(0, n_seqs))
-        if op == 0:                                            # append S tokens, both layers
-            S = int(rng.integers(1, 2 * B + 5))
-            if int(opool.lens[s]) + S > mbps * B:
+        if op == 0:                          # append S_i tokens to 1-3 sequences in one call, both layers
+            seqs = rng.choice(n_seqs, size=int(rng.integers(1, 4)), replace=False).tolist()
+            sizes = [int(rng.integers(1, 2 * B + 5)) for _ in seqs]
+            if any(int(opool.lens[q]) + S > mbps * B for q, S in zip(seqs, sizes)):
                 continue
-            need = -(-(int(opool.lens[s]) + S) // B) - int(opool.nalloc[s]) + (1 if opool._shared_tail(s, S) else 0)
-            if need > opool.top:
-                continue
-            P = int(opool.lens[s])
-            assert opool.reserve([s], [S]) == 0
+            starts = [int(opool.lens[q]) for q in seqs]
+            rc_o = opool.reserve(seqs, sizes)
+            T = sum(sizes)
             for layer in range(layers):
-                k = rng.standard_normal((S, 2, 64)).astype(np.float32)
-                v = rng.standard_normal((S, 2, 64)).astype(np.float32)
-                q = rng.standard_normal((S, 4, 64)).astype(np.float32)
-                opool.write(layer, s, P, k.astype(np.float64), v.astype(np.float64))
-                o = torch.empty((S, 4, 64), device="cuda")
-                rc = pool.replay(layer, [s], [S], dev(q, "f32"), dev(k, "f32"), dev(v, "f32"), o,
+                k = rng.standard_normal((T, 2, 64)).astype(np.float32)
+                v = rng.standard_normal((T, 2, 64)).astype(np.float32)
+                q = rng.standard_normal((T, 4, 64)).astype(np.float32)
+                o = torch.empty((T, 4, 64), device="cuda")
+                rc = pool.replay(layer, seqs, sizes, dev(q, "f32"), dev(k, "f32"), dev(v, "f32"), o,
                                  0.125, commit=layer == layers - 1)
-                assert rc == 0, rc
-            opool.commit([s], [S])
+                assert rc == rc_o, (rc, rc_o)                      # ENOMEM on both sides, or neither
+                if rc:
+                    break
+                off = 0
+                for qs, P, S in zip(seqs, starts, sizes):
+                    opool.write(layer, qs, P, k[off:off + S].astype(np.float64), v[off:off + S].astype(np.float64))
+                    off += S
+            if rc_o == 0:
+                opool.commit(seqs, sizes)
         elif op == 1:                                          # crop
             L = int(rng.integers(0, int(opool.lens[s]) + 1))
             assert opool.crop([s], [L]) == 0
