@@ -409,13 +409,20 @@ def bench_decode(args):
     sequence per step: reserve + append, split-key decode attention over the
     whole cache, then seeded Gumbel-max sampling (T = 0.7) over a 128256-entry
     vocabulary of synthetic logits (the LM head is not on this path).  The
-    roofline is HBM: K/V bytes one step must read over the attention time."""
+    roofline is HBM: K/V bytes one step must read over the attention time.
+    The ``_fp8`` workload keeps the cache as E4M3 codes (one byte per value,
+    per-layer scales 5/448: N(0, 1) values up to 5 sigma use the full range)."""
     import torch
-    from paper_2609_04875_amd import BF16, KVPool, sample_tokens, sample_workspace_bytes, workspace_bytes
+    from paper_2609_04875_amd import BF16, FP8_E4M3, KVPool, sample_tokens, sample_workspace_bytes, workspace_bytes
+    fp8 = args.workload.endswith("_fp8")
     n, ctx, hq, hkv, d, B, vocab, T = 32, 8192, 32, 8, 128, 16, 128256, 0.7
+    kv_elem = 1 if fp8 else 2
     total = args.warmup + args.steps
     bps = (ctx + total) // B + 2
-    pool = KVPool(1, hq, hkv, d, n * bps + 8, n, bps, BF16, B, workspace_bytes=workspace_bytes(hq, d, n, 32))
+    pool = KVPool(1, hq, hkv, d, n * bps + 8, n, bps, FP8_E4M3 if fp8 else BF16, B,
+                  workspace_bytes=workspace_bytes(hq, d, n, 32))
+    if fp8:
+        pool.set_kv_scales([5.0 / 448], [5.0 / 448])
     g = torch.Generator(device="cuda").manual_seed(7)
     rnd = lambda *shape: torch.randn(*shape, device="cuda", generator=g).to(torch.bfloat16)
     keep = None
@@ -445,7 +452,7 @@ def bench_decode(args):
             step_ms.append(ev[0].elapsed_time(ev[2]))
             samp_ms.append(ev[1].elapsed_time(ev[2]))
             attn_ms.append(pool.last_times()[1])
-            kv_bytes.append(n * (ctx + t + 1) * hkv * d * 2 * 2 + 2 * n * hq * d * 2)
+            kv_bytes.append(n * (ctx + t + 1) * hkv * d * 2 * kv_elem + 2 * n * hq * d * 2)
     if args.calibrate_copy_mib:
         copy_calibration(args.calibrate_copy_mib)
     a_ms = float(np.mean(attn_ms))
@@ -456,13 +463,13 @@ def bench_decode(args):
         "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": total_s * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "decode_llama8b_b32_ctx8192", "sequences": n, "context": ctx,
+        "config": {"workload": args.workload, "sequences": n, "context": ctx,
                    "n_q_heads": hq, "n_kv_heads": hkv, "head_dim": d, "block_size": B, "vocab": vocab,
-                   "temperature": T},
+                   "temperature": T, "kv_cache": "e4m3" if fp8 else "bf16"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": 8000.0, "unit": "GB/s",
                      "frac": achieved / 8000.0,
-                     "traffic": measured_traffic("attn_bf16", "decode_llama8b_b32_ctx8192"),
-                     "kernel": "attn_bf16_kernel<128,4,16> + split_combine_kernel<128>",
+                     "traffic": measured_traffic("attn_bf16", args.workload),
+                     "kernel": f"attn_bf16_kernel<128,4,16,{'fp8' if fp8 else 'bf16'}> + split_combine_kernel<128>",
                      "kernel_ms": a_ms, "kernel_launches_per_step": 1,
                      "algorithmic_bytes_per_step": float(np.mean(kv_bytes))},
         "breakdown_ms": {"attention": a_ms, "sampling": float(np.mean(samp_ms)),
