@@ -468,8 +468,8 @@ def bench_decode(args):
                    "temperature": T, "kv_cache": "e4m3" if fp8 else "bf16"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": 8000.0, "unit": "GB/s",
                      "frac": achieved / 8000.0,
-                     "traffic": measured_traffic("attn_bf16", args.workload),
-                     "kernel": f"attn_bf16_kernel<128,4,16,{'fp8' if fp8 else 'bf16'}> + split_combine_kernel<128>",
+                     "traffic": measured_traffic("attn_decode", args.workload),
+                     "kernel": f"attn_decode_kernel<128,16,{'fp8' if fp8 else 'bf16'}> + split_combine_kernel<128>",
                      "kernel_ms": a_ms, "kernel_launches_per_step": 1,
                      "algorithmic_bytes_per_step": float(np.mean(kv_bytes))},
         "breakdown_ms": {"attention": a_ms, "sampling": float(np.mean(samp_ms)),

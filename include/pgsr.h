@@ -185,8 +185,13 @@ int pgsr_kv_fork(pgsr_pool *pool, int32_t n, const int32_t *srcs, const int32_t 
  * q_lens: HOST arrays.
  * flags & PGSR_COMMIT adds S_i to each length (set it on the last layer of a
  * step) and sum S_i to *recomputed_tokens (HOST, nullable) -- the count of
- * Corollary 1.  Outputs are bitwise reproducible run to run and depend only on
- * each query's absolute position, not on how the suffix is batched.
+ * Corollary 1.  Outputs are bitwise reproducible run to run.  On a pool
+ * without a workspace they depend only on each query's absolute position, not
+ * on how the suffix is batched.  With a workspace, a call that would leave
+ * compute units idle splits keys over several workgroups, and a call whose
+ * sequences all have at most 32 / (n_q_heads / n_kv_heads) query tokens (a
+ * decode step) runs a decode kernel; both round in another order, so their
+ * bits depend on the call's shape as well.
  */
 int pgsr_replay_prefill(pgsr_pool *pool, int32_t layer, int32_t n, const int32_t *seqs,
                         const int32_t *q_lens, const void *q, const void *k, const void *v,

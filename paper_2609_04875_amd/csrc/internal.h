@@ -169,6 +169,11 @@ hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 // Same kernel over an FP8 E4M3 cache: codes widen to bf16 exactly on the way
 // into LDS; the K scale is in scale_log2, the V scale in o_scale.
 hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s);
+// Decode attention (every sequence of the launch has at most 32 / G query
+// tokens): one wave per (sequence, KV head, split) gathering MFMA operands from
+// the cache without LDS; with n_splits > 1 it writes split partials.
+hipError_t launch_attn_decode(const AttnArgs& a, bool fp8, hipStream_t s);
+int attn_decode_keys_per_tile();
 // Merge split-key partials into O (bf16), splits in increasing order.
 hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,

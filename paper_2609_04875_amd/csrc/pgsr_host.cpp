@@ -189,6 +189,18 @@ struct Seg {
 constexpr int64_t kSplitTargetWorkgroups = 512;
 constexpr int64_t kMaxSplits = 32;
 constexpr int32_t kSplitAlign = 64;
+// Decode kernel (calls whose sequences all fit one wave's 32 query rows, with
+// a workspace): aim for eight waves per CU, at most 64 splits of at least 256
+// keys each.
+#ifndef PGSR_DECODE_TARGET_WAVES
+#define PGSR_DECODE_TARGET_WAVES 2048
+#endif
+#ifndef PGSR_DECODE_MIN_SPLIT_KEYS
+#define PGSR_DECODE_MIN_SPLIT_KEYS 256
+#endif
+constexpr int64_t kDecodeTargetWaves = PGSR_DECODE_TARGET_WAVES;
+constexpr int64_t kDecodeMaxSplits = 64;
+constexpr int32_t kDecodeMinSplitKeys = PGSR_DECODE_MIN_SPLIT_KEYS;
 
 // Validation of a replay step: lengths, table width, free blocks.
 int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
@@ -315,6 +327,10 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
   }
   // Attention, chunked; within a launch, costlier sequences first.
   const int group = p->hq / p->hkv;
+  // Decode path: every sequence's queries fit one wave (32 / G tokens) and the
+  // pool has a workspace (so batching already decides the rounding order).
+  bool decode = p->dtype != PGSR_F32 && p->workspace != nullptr;
+  for (const Seg& g : segs) decode = decode && g.q_len <= 32 / group;
   const int tile_tokens = p->dtype == PGSR_F32 ? attn_f32_tile_tokens(p->d, group)
                                                 : attn_bf16_tile_tokens(p->d, group);
   for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
@@ -354,6 +370,28 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.n_splits = 1;
     a.split_len = 0;
     a.n_rows = off * p->hq;                        // packed query rows of the whole call
+    if (decode) {
+      int32_t max_key = 0;
+      for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);
+      const int64_t units = (int64_t)cnt * p->hkv;
+      const int64_t per_split = (int64_t)a.n_rows * ((int64_t)p->d + 2) * (int64_t)sizeof(float);
+      int64_t ns = (kDecodeTargetWaves + units - 1) / units;
+      ns = std::min<int64_t>(ns, kDecodeMaxSplits);
+      ns = std::min<int64_t>(ns, std::max<int64_t>(1, max_key / kDecodeMinSplitKeys));
+      ns = std::min<int64_t>(ns, (int64_t)(p->workspace_bytes / std::max<int64_t>(per_split, 1)));
+      if (ns > 1) {
+        const int32_t kt = attn_decode_keys_per_tile();
+        const int32_t len = cdiv(cdiv(max_key, ns), kt) * kt;
+        a.n_splits = cdiv(max_key, len);
+        a.split_len = len;
+        a.ws_acc = (float*)p->workspace;
+        a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
+      }
+      hipError_t err = launch_attn_decode(a, p->dtype == PGSR_FP8_E4M3, st);
+      if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine_bf16(a, st);
+      if (err != hipSuccess) return hip_fail(err, "decode attention launch");
+      continue;
+    }
     // Split-key mode when the launch would leave CUs idle and the caller gave
     // a workspace for the partials: splits at absolute multiples of split_len.
     const int64_t wgs = (int64_t)tiles * p->hkv;

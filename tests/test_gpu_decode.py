@@ -99,3 +99,49 @@ def test_decode_is_bitwise_reproducible():
     assert pool.crop([0, 1], [ep.prefix for ep in eps]) == 0
     again = _decode(pool, eps, [0, 1], 2)
     assert torch.equal(first, again)
+
+
+DEC_CASES = [
+    # geometry, block size, prefixes, query tokens per sequence (<= 32 / G: the decode kernel)
+    (W.AttnGeometry(32, 8, 128), 16, (0, 5, 100, 1000, 3001), (1, 8, 3, 8, 5)),
+    (W.AttnGeometry(28, 4, 128), 32, (31, 777, 2047), (4, 1, 3)),
+    (W.AttnGeometry(16, 4, 64), 64, (64, 500, 4000), (7, 2, 8)),
+    (W.AttnGeometry(8, 8, 64), 16, (17, 1300), (32, 29)),
+]
+
+
+@pytest.mark.parametrize("case", range(len(DEC_CASES)))
+def test_decode_kernel_multi_token_over_poisoned_tails(case):
+    """Several query tokens per sequence (causal among themselves) after a crop
+    that NaN-fills the released slots: with a workspace the call runs the decode
+    kernel (one wave per sequence, KV head and split), without one the prefill
+    kernel; both match the oracle, so no stale slot reaches the result."""
+    geom, B, prefixes, q_lens = DEC_CASES[case]
+    log(f"decode kernel case {case}: {geom} B={B} prefixes={prefixes} q_lens={q_lens}")
+    rng = np.random.default_rng(300 + case)
+    eps = [W.draw_episode(rng, geom, "bf16", P, S, P + S + 37) for P, S in zip(prefixes, q_lens)]
+    n = len(eps)
+    nb = sum(-(-ep.t_contaminated // B) + 2 for ep in eps)
+    bps = max(-(-ep.t_contaminated // B) for ep in eps) + 1
+    scale = geom.head_dim ** -0.5
+    seqs = list(range(n))
+    cat = lambda f: torch.cat([dev(f(ep), "bf16") for ep in eps])
+    outs = []
+    for split_q in (sum(q_lens), 0):
+        pool = make_pool(geom, "bf16", nb, n, bps, block_size=B, split_q=split_q, max_splits=64)
+        cq, ck, cv = (cat(lambda ep, x=x: ep.contaminated(x)) for x in ("q", "k", "v"))
+        assert pool.replay(0, seqs, [ep.t_contaminated for ep in eps], cq, ck, cv, torch.empty_like(cq), scale) == 0
+        assert pool.crop(seqs, [ep.prefix for ep in eps], poison=True) == 0
+        q, k, v = (cat(lambda ep, x=x: getattr(ep, x)[ep.prefix:]) for x in ("q", "k", "v"))
+        o = torch.empty_like(q)
+        assert pool.replay(0, seqs, list(q_lens), q, k, v, o, scale) == 0
+        outs.append(o.float().cpu().numpy())
+    off = 0
+    for i, ep in enumerate(eps):
+        ref = oracle.attention(storage_f64(ep.q[ep.prefix:], "bf16"), storage_f64(ep.k, "bf16"),
+                               storage_f64(ep.v, "bf16"), ep.prefix, scale)
+        for name, o in zip(("decode kernel", "prefill kernel"), outs):
+            got = o[off:off + ep.suffix]
+            assert np.isfinite(got).all(), f"{name} seq {i}"
+            assert_close(got, ref, "bf16", f"{name} seq {i}")
+        off += ep.suffix
