@@ -72,8 +72,11 @@ class Setup:
         nb = sum(-(-e.t_contaminated // B) + -(-e.t_sanitized // B) for e in self.eps) + 8
         max_bps = max(-(-max(e.t_contaminated, e.t_sanitized) // B) for e in self.eps) + 4
         # workspace for split-key launches (partial softmax states) where a
-        # replay call is too small to fill the GPU: the chunked workload
-        ws = workspace_bytes(g.n_q_heads, g.head_dim, self.chunk) if self.chunk else 0
+        # replay call is too small to fill the GPU: the chunked workload and
+        # the tiny fp32 one (larger calls never split, so they get none)
+        small = sum(e.suffix for e in self.eps) * g.n_q_heads < 1 << 15
+        ws = workspace_bytes(g.n_q_heads, g.head_dim, self.chunk or sum(e.suffix for e in self.eps)) \
+            if (self.chunk or small) else 0
         self.pool = KVPool(1, g.n_q_heads, g.n_kv_heads, g.head_dim, nb, len(self.eps), max_bps,
                            F32 if w.dtype == "f32" else BF16, B, workspace_bytes=ws)
         dev = lambda a: self._dev(a)
@@ -275,11 +278,9 @@ def traffic_profile_path(kernel_file: str, workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"{kernel_file}_{short}_traffic.json")
 
 
-def measured_traffic(kernel_file: str, workload: str):
-    """HBM bytes per step of the dominant kernel (FETCH_SIZE and WRITE_SIZE,
-    each scaled by what it reads for a plain copy of known size), from the
-    committed counter summary; None when there is none for this workload or
-    the kernel source changed since the counters were taken."""
+def _profile_record(kernel_file: str, workload: str):
+    """The committed counter summary of the dominant kernel on ``workload``, or
+    None when there is none or the kernel source changed since it was taken."""
     import hashlib
     path = traffic_profile_path(kernel_file, workload)
     if not os.path.exists(path):
@@ -289,7 +290,24 @@ def measured_traffic(kernel_file: str, workload: str):
     with open(os.path.join(ROOT, rec["kernel_source"]), "rb") as f:
         if hashlib.sha256(f.read()).hexdigest() != rec["kernel_source_sha256"]:
             return None
-    return rec["traffic_bytes_per_step"]
+    return rec
+
+
+def measured_traffic(kernel_file: str, workload: str):
+    """HBM bytes per step of the dominant kernel (FETCH_SIZE and WRITE_SIZE,
+    each scaled by what it reads for a plain copy of known size), from the
+    committed counter summary; None when there is none for this workload or
+    the kernel source changed since the counters were taken."""
+    rec = _profile_record(kernel_file, workload)
+    return None if rec is None else rec["traffic_bytes_per_step"]
+
+
+def measured_sclk(kernel_file: str, workload: str):
+    """Mean shader clock (GHz) over the dominant kernel's dispatches in the
+    committed counter summary (GRBM_GUI_ACTIVE summed over the 8 XCDs, divided
+    by 8 and by the dispatch duration), or None."""
+    rec = _profile_record(kernel_file, workload)
+    return None if rec is None else rec.get("sclk_ghz")
 
 
 def copy_calibration(mib: int) -> None:
@@ -623,6 +641,12 @@ def main() -> int:
     attn_mean = float(np.mean(attn_ms))
     achieved = flops / (attn_mean * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
+    kfile = "attn_bf16" if w.dtype == "bf16" else "attn_f32"
+    sclk = measured_sclk(kfile, w.name)
+    # crop: released table entries (each read, cleared, its count read and
+    # written, then pushed) plus lengths and the stack top
+    released = sum(-(-e.t_contaminated // w.block_size) - -(-e.prefix // w.block_size) for e in st.eps)
+    crop_bytes = 20 * released + 4 * len(st.eps) + 4
     result = {
         "metric": METRIC,
         "value": tokens / total_s,
@@ -644,12 +668,18 @@ def main() -> int:
                    "recomputed_tokens": sum(st.S)},
         "roofline": {"bound": "mfma" if w.dtype == "bf16" else "alu", "achieved": achieved,
                      "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": measured_traffic("attn_bf16" if w.dtype == "bf16" else "attn_f32", w.name),
+                     "traffic": measured_traffic(kfile, w.name),
+                     # the clock the kernel actually ran at (counter summary) and the
+                     # fraction of the peak at that clock (peak scales with sclk / 2.4)
+                     "sclk_ghz": sclk,
+                     "frac_at_sclk": None if sclk is None else achieved / (peak * sclk / 2.4),
                      "kernel": ("attn_bf16_kernel<128,4,16>" if w.dtype == "bf16"
                                 else f"attn_f32_kernel<{g.head_dim}>"),
                      "flops_per_step": flops, "algorithmic_bytes_per_step": nbytes,
                      "kernel_ms": attn_mean, "kernel_launches_per_step": st.calls_per_step,
                      "algorithmic_GBps": nbytes / (attn_mean * 1e-3) / 1e9},
+        "crop": {"us": float(np.mean(crop_ms)) * 1e3, "algorithmic_bytes": crop_bytes,
+                 "released_blocks": released},
         "breakdown_ms": {"crop": float(np.mean(crop_ms)), "append": float(np.mean(append_ms)),
                          "attention": attn_mean, "step": total_s * 1e3 / args.steps,
                          "step_min": float(np.min(step_ms))},

@@ -372,8 +372,8 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
 // the sums still run in increasing s.
 constexpr int kGroup = 8;
 
-template <int D>
-__global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t* __restrict__ og) {
+template <int D, typename TO>
+__global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, TO* __restrict__ og) {
   constexpr int TPR = D / 8;                       // threads per row
   const int64_t row = (int64_t)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
   const int c0 = (threadIdx.x % TPR) * 8;
@@ -420,13 +420,18 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, uint16_t
     }
   }
   const float inv = a.o_scale / L;
-  bf16x8 out;
+  if constexpr (std::is_same_v<TO, float>) {       // fp32 pools
+    *(f32x4*)(og + row * D + c0) = o0 * inv;
+    *(f32x4*)(og + row * D + c0 + 4) = o1 * inv;
+  } else {
+    bf16x8 out;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    out[j] = (__bf16)(o0[j] * inv);
-    out[4 + j] = (__bf16)(o1[j] * inv);
+    for (int j = 0; j < 4; ++j) {
+      out[j] = (__bf16)(o0[j] * inv);
+      out[4 + j] = (__bf16)(o1[j] * inv);
+    }
+    *(bf16x8*)(og + row * D + c0) = out;
   }
-  *(bf16x8*)(og + row * D + c0) = out;
 }
 
 }  // namespace
@@ -453,14 +458,18 @@ static hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s) {
   if (a.n_rows <= 0) return hipSuccess;
   const int rows_per_block = 256 / (a.head_dim / 8);
   dim3 grid((a.n_rows + rows_per_block - 1) / rows_per_block);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(split_combine_kernel<128>, grid, dim3(256), 0, s, a, (uint16_t*)a.o);
+  if (a.head_dim == 128 && f32_out)
+    hipLaunchKernelGGL((split_combine_kernel<128, float>), grid, dim3(256), 0, s, a, (float*)a.o);
+  else if (a.head_dim == 64 && f32_out)
+    hipLaunchKernelGGL((split_combine_kernel<64, float>), grid, dim3(256), 0, s, a, (float*)a.o);
+  else if (a.head_dim == 128)
+    hipLaunchKernelGGL((split_combine_kernel<128, uint16_t>), grid, dim3(256), 0, s, a, (uint16_t*)a.o);
   else if (a.head_dim == 64)
-    hipLaunchKernelGGL(split_combine_kernel<64>, grid, dim3(256), 0, s, a, (uint16_t*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<64, uint16_t>), grid, dim3(256), 0, s, a, (uint16_t*)a.o);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

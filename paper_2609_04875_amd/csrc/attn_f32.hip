@@ -16,6 +16,11 @@
 // key-major without padding, read as 16-byte broadcasts (every lane reads the
 // same key).  This path exists for fp32 accuracy (1e-4 against fp64); the
 // bf16 MFMA kernel is the performance path.
+//
+// Split-key mode (a call too small to fill the chip, with a workspace): split
+// s of a query tile covers the keys [s * split_len, (s+1) * split_len) at
+// absolute positions and writes its merged unnormalised state (m, l, acc) in
+// fp32 for the split combine, which adds the splits in increasing order.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -36,7 +41,8 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
   constexpr int KV = KT * D;                      // floats per tile operand
   __shared__ __attribute__((aligned(16))) float lds[kWaves][2][KV];
 
-  const int tile = blockIdx.x;
+  const int tile = blockIdx.x / a.n_splits;
+  const int split = blockIdx.x % a.n_splits;
   const int hq = blockIdx.y;
   int ei = 0;
   while (ei + 1 < a.n && a.e[ei + 1].tile_start <= tile) ++ei;
@@ -51,7 +57,13 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
   const int qpos = valid ? e.prefix + t : -1;    // absolute position (-1: padding row)
   const int t_last = min(e.q_len, (lt + 1) * kTokens) - 1;
   const int kv_len = e.prefix + e.q_len;
-  const int n_kt = (e.prefix + t_last + 1 + KT - 1) / KT;   // tiles covering keys [0, key_end)
+  // keys this workgroup visits: [key_lo, key_end), whole tiles at absolute
+  // positions (split_len is a multiple of KT)
+  const int key_lo = a.n_splits > 1 ? split * a.split_len : 0;
+  const int key_end = a.n_splits > 1 ? min(e.prefix + t_last + 1, key_lo + a.split_len) : e.prefix + t_last + 1;
+  if (key_lo >= key_end) return;                   // the whole workgroup: no barrier is skipped
+  const int kt0 = key_lo / KT;
+  const int n_kt = (key_end + KT - 1) / KT;
 
   float qr[D];
   {
@@ -75,7 +87,7 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
   float* ks = lds[w][0];
   float* vs = lds[w][1];
 
-  for (int kt = w; kt < n_kt; kt += kWaves) {
+  for (int kt = kt0 + w; kt < n_kt; kt += kWaves) {
     const int kb = kt * KT;
     // K: slot rows of D floats, 4 at a time
     for (int i = lane; i < KV / 4; i += 64) {
@@ -119,7 +131,7 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
         d0 = fmaf(qr[c + 2], kv[2], d0);
         d1 = fmaf(qr[c + 3], kv[3], d1);
       }
-      s[j] = (kb + j <= qpos) ? (d0 + d1) * c2 : -INFINITY;
+      s[j] = (kb + j <= qpos && kb + j < key_end) ? (d0 + d1) * c2 : -INFINITY;
       tmax = fmaxf(tmax, s[j]);
     }
     const float m_new = fmaxf(m, tmax);
@@ -173,7 +185,14 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
       m = mn;
     }
   }
-  if (w == 0 && valid) {
+  if (w == 0 && valid && a.n_splits > 1) {        // unnormalised partials
+    const int64_t prow = (int64_t)split * a.n_rows + (int64_t)(e.q_off + t) * a.n_q_heads + hq;
+    float* acc_out = a.ws_acc + prow * D;
+#pragma unroll
+    for (int c = 0; c < D; c += 4) *(f32x4*)(acc_out + c) = f32x4{acc[c], acc[c + 1], acc[c + 2], acc[c + 3]};
+    a.ws_ml[2 * prow] = m;
+    a.ws_ml[2 * prow + 1] = l;
+  } else if (w == 0 && valid) {
     float* op = (float*)a.o + ((int64_t)(e.q_off + t) * a.n_q_heads + hq) * D;
     const float inv = 1.f / l;
 #pragma unroll
@@ -188,7 +207,7 @@ int attn_f32_tile_tokens(int, int) { return kTokens; }
 
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
-  dim3 grid(a.n_tiles, a.n_q_heads);
+  dim3 grid(a.n_tiles * a.n_splits, a.n_q_heads);
   if (a.head_dim == 64)
     hipLaunchKernelGGL((attn_f32_kernel<64, 32>), grid, dim3(kWaves * 64), 0, s, a);
   else if (a.head_dim == 128)

@@ -174,8 +174,9 @@ hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s);
 // the cache without LDS; with n_splits > 1 it writes split partials.
 hipError_t launch_attn_decode(const AttnArgs& a, bool fp8, hipStream_t s);
 int attn_decode_keys_per_tile();
-// Merge split-key partials into O (bf16), splits in increasing order.
-hipError_t launch_split_combine_bf16(const AttnArgs& a, hipStream_t s);
+// Merge split-key partials into O (bf16, or fp32 for fp32 pools), splits in
+// increasing order.
+hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
                             int32_t* free_list, int32_t n_blocks, int32_t* free_top, int32_t* refs,
                             hipStream_t s);

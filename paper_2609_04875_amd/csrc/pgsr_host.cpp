@@ -388,14 +388,16 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
       hipError_t err = launch_attn_decode(a, p->dtype == PGSR_FP8_E4M3, st);
-      if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine_bf16(a, st);
+      if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine(a, false, st);
       if (err != hipSuccess) return hip_fail(err, "decode attention launch");
       continue;
     }
     // Split-key mode when the launch would leave CUs idle and the caller gave
     // a workspace for the partials: splits at absolute multiples of split_len.
-    const int64_t wgs = (int64_t)tiles * p->hkv;
-    if (p->dtype != PGSR_F32 && p->workspace && wgs < kSplitTargetWorkgroups) {
+    // (the bf16 kernel packs a KV head's query heads into one workgroup, the
+    // fp32 kernel takes one query head per workgroup)
+    const int64_t wgs = (int64_t)tiles * (p->dtype == PGSR_F32 ? p->hq : p->hkv);
+    if (p->workspace && wgs < kSplitTargetWorkgroups) {
       int32_t max_key = 0;
       for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);
       const int64_t per_split = (int64_t)a.n_rows * ((int64_t)p->d + 2) * (int64_t)sizeof(float);
@@ -412,7 +414,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     hipError_t err = p->dtype == PGSR_F32    ? launch_attn_f32(a, st)
                      : p->dtype == PGSR_BF16 ? launch_attn_bf16(a, st)
                                              : launch_attn_fp8(a, st);
-    if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine_bf16(a, st);
+    if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine(a, p->dtype == PGSR_F32, st);
     if (err != hipSuccess) return hip_fail(err, "attention launch");
   }
 

@@ -98,3 +98,28 @@ def test_long_horizon_split_full_size_sampled():
     rows = np.unique(np.concatenate([toks * 32 + rng.integers(0, 32, toks.shape[0]), toks * 32 + 31]))
     ref = oracle_suffix(ep, w.scale, rows=rows)
     assert_close(o.float().cpu().numpy().reshape(-1, 128)[rows], ref, "bf16", w.name)
+
+
+@pytest.mark.parametrize("geom,P,S", [(W.AttnGeometry(8, 8, 64), 512, 128), (W.AttnGeometry(4, 2, 128), 301, 70),
+                                      (W.AttnGeometry(8, 8, 64), 0, 100)])
+def test_fp32_split_replay_matches_oracle(geom, P, S):
+    """fp32 pools split keys too when a call launches few workgroups (the tiny
+    workload: 2 query tiles x 8 heads); partials merge into fp32 output within
+    the fp32 tolerance."""
+    log(f"fp32 split {geom} P={P} S={S}")
+    rng = np.random.default_rng(P + 7 * S)
+    ep = W.draw_episode(rng, geom, "f32", P, S, P + 33)
+    scale = geom.head_dim ** -0.5
+    nb = _blocks(P + S + 33) + _blocks(P + S) + 4
+    outs = []
+    for split_q in (S, 0):
+        pool = make_pool(geom, "f32", nb, 1, 64, split_q=split_q)
+        contaminated_then_crop(pool, ep, 0, scale, poison=True)
+        q, k, v = (dev(getattr(ep, x)[ep.prefix:], "f32") for x in ("q", "k", "v"))
+        o = torch.empty_like(q)
+        assert pool.replay(0, [0], [S], q, k, v, o, scale) == 0
+        outs.append(o)
+    ref = oracle_suffix(ep, scale)
+    assert_close(outs[0].cpu().numpy(), ref, "f32", "split")
+    assert_close(outs[1].cpu().numpy(), ref, "f32", "plain")
+    assert not torch.equal(outs[0], outs[1])
