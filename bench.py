@@ -576,6 +576,8 @@ def main() -> int:
     ap.add_argument("--workload", default=DEFAULT)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--prefill-kernel", choices=("auto", "four_wave"), default="auto",
+                    help="bf16 prefill kernel: pipelined where it applies (auto) or four-wave")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device (counter scaling)")
     args = ap.parse_args()
@@ -598,6 +600,9 @@ def main() -> int:
         return bench_decoder(args)
     st = Setup(args.workload)
     w, g, pool = st.w, st.w.geometry, st.pool
+    pool.set_prefill_kernel(args.prefill_kernel)
+    pipe = (w.dtype == "bf16" and args.prefill_kernel == "auto" and g.head_dim == 128
+            and 32 % (g.n_q_heads // g.n_kv_heads) == 0)
     single_call = st.calls_per_step == 1
     pool.enable_timing(single_call)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -641,7 +646,7 @@ def main() -> int:
     attn_mean = float(np.mean(attn_ms))
     achieved = flops / (attn_mean * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
-    kfile = "attn_bf16" if w.dtype == "bf16" else "attn_f32"
+    kfile = ("attn_bf16_pipe" if pipe else "attn_bf16") if w.dtype == "bf16" else "attn_f32"
     sclk = measured_sclk(kfile, w.name)
     # crop: released table entries (each read, cleared, its count read and
     # written, then pushed) plus lengths and the stack top
@@ -673,7 +678,8 @@ def main() -> int:
                      # fraction of the peak at that clock (peak scales with sclk / 2.4)
                      "sclk_ghz": sclk,
                      "frac_at_sclk": None if sclk is None else achieved / (peak * sclk / 2.4),
-                     "kernel": ("attn_bf16_kernel<128,4,16>" if w.dtype == "bf16"
+                     "kernel": ("attn_bf16_pipe_kernel<16>" if pipe
+                                else f"attn_bf16_kernel<{g.head_dim},4,16>" if w.dtype == "bf16"
                                 else f"attn_f32_kernel<{g.head_dim}>"),
                      "flops_per_step": flops, "algorithmic_bytes_per_step": nbytes,
                      "kernel_ms": attn_mean, "kernel_launches_per_step": st.calls_per_step,

@@ -220,6 +220,18 @@ int pgsr_pool_enable_timing(pgsr_pool *pool, int on);
 int pgsr_pool_last_times(pgsr_pool *pool, float *append_ms, float *attention_ms);
 
 /*
+ * Choice of the bf16 prefill attention kernel (Algorithm 1 replay loop,
+ * prefill form).  PGSR_PREFILL_AUTO (the default) runs the software-pipelined
+ * kernel (one wave per SIMD, 64 query rows per wave) wherever it applies:
+ * head_dim 128, a GQA group dividing 32, a bf16 pool; every other call runs
+ * the four-wave kernel.  PGSR_PREFILL_FOUR_WAVE runs the four-wave kernel for
+ * every call.  Both give identical bits for every query row; the option only
+ * moves time.  Host only, no device work; EINVAL for another value.
+ */
+enum { PGSR_PREFILL_AUTO = 0, PGSR_PREFILL_FOUR_WAVE = 1 };
+int pgsr_pool_set_prefill_kernel(pgsr_pool *pool, int kind);
+
+/*
  * Dense projection of the stacked-layer transition F (theta in Eq. (1)):
  * Y[m][n] = sum_k X[m][k] * W[n][k] (+ R[m][n] when R != NULL), i.e. Y = X W^T
  * with W in the linear-layer layout [n][k]; bf16 row-major device arrays,

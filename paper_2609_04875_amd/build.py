@@ -27,6 +27,13 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+# Per-source options.  The pipelined prefill kernel runs one wave per SIMD and
+# reads every product's result with VALU instructions (softmax, rescale), so
+# its matrix results must live in VGPRs: left to its heuristics the compiler
+# places them in AGPRs and copies them back on every step.
+EXTRA = {"attn_bf16_pipe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
@@ -34,7 +41,8 @@ def sources():
 def _compile(src: str, verbose: bool, objdir: str = OBJDIR, defines=()) -> str:
     obj = os.path.join(objdir, os.path.basename(src) + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC, *COMMON, *[f"-D{d}" for d in defines], *lang, "-c", src, "-o", obj]
+    extra = EXTRA.get(os.path.basename(src), [])
+    cmd = [HIPCC, *COMMON, *extra, *[f"-D{d}" for d in defines], *lang, "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -166,6 +166,11 @@ hipError_t launch_fork(const ForkArgs& a, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
+// Software-pipelined bf16 prefill for head_dim 128 and GQA groups dividing
+// 32: one wave per SIMD, 64 query rows per wave, one workgroup per CU.
+bool attn_bf16_pipe_eligible(int head_dim, int group);
+int attn_bf16_pipe_tile_tokens(int group);
+hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s);
 // Same kernel over an FP8 E4M3 cache: codes widen to bf16 exactly on the way
 // into LDS; the K scale is in scale_log2, the V scale in o_scale.
 hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s);

@@ -43,6 +43,8 @@ struct pgsr_pool {
   bool timing = false, timed_call = false;
   // FP8 pools: per-layer K and V scales (stored code = x / scale, read = code * scale)
   std::vector<float> k_scale, v_scale;
+  // bf16 prefill kernel choice (PGSR_PREFILL_AUTO / PGSR_PREFILL_FOUR_WAVE)
+  int prefill_kind = PGSR_PREFILL_AUTO;
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
 };
 
@@ -187,6 +189,8 @@ struct Seg {
 // (a decode step of one sequence, 8 workgroups unsplit, then fills the chip),
 // split boundaries at multiples of the 64-key tile.
 constexpr int64_t kSplitTargetWorkgroups = 512;
+// The pipelined bf16 kernel holds a CU alone (one wave per SIMD).
+constexpr int64_t kSplitTargetWorkgroupsPipe = 256;
 constexpr int64_t kMaxSplits = 32;
 constexpr int32_t kSplitAlign = 64;
 // Decode kernel (calls whose sequences all fit one wave's 32 query rows, with
@@ -331,8 +335,11 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
   // pool has a workspace (so batching already decides the rounding order).
   bool decode = p->dtype != PGSR_F32 && p->workspace != nullptr;
   for (const Seg& g : segs) decode = decode && g.q_len <= 32 / group;
+  const bool pipe = p->dtype == PGSR_BF16 && p->prefill_kind == PGSR_PREFILL_AUTO &&
+                    attn_bf16_pipe_eligible(p->d, group);
   const int tile_tokens = p->dtype == PGSR_F32 ? attn_f32_tile_tokens(p->d, group)
-                                                : attn_bf16_tile_tokens(p->d, group);
+                          : pipe               ? attn_bf16_pipe_tile_tokens(group)
+                                               : attn_bf16_tile_tokens(p->d, group);
   for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
     const int32_t cnt = (int32_t)std::min<size_t>(kMaxSeqsPerLaunch, segs.size() - base);
     std::vector<Seg> chunk(segs.begin() + base, segs.begin() + base + cnt);
@@ -397,11 +404,12 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     // (the bf16 kernel packs a KV head's query heads into one workgroup, the
     // fp32 kernel takes one query head per workgroup)
     const int64_t wgs = (int64_t)tiles * (p->dtype == PGSR_F32 ? p->hq : p->hkv);
-    if (p->workspace && wgs < kSplitTargetWorkgroups) {
+    const int64_t target = pipe ? kSplitTargetWorkgroupsPipe : kSplitTargetWorkgroups;
+    if (p->workspace && wgs < target) {
       int32_t max_key = 0;
       for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);
       const int64_t per_split = (int64_t)a.n_rows * ((int64_t)p->d + 2) * (int64_t)sizeof(float);
-      int64_t ns = std::min<int64_t>(kMaxSplits, (kSplitTargetWorkgroups + wgs - 1) / wgs);
+      int64_t ns = std::min<int64_t>(kMaxSplits, (target + wgs - 1) / wgs);
       ns = std::min<int64_t>(ns, (int64_t)(p->workspace_bytes / std::max<int64_t>(per_split, 1)));
       if (ns > 1) {
         const int32_t len = cdiv(cdiv(max_key, ns), kSplitAlign) * kSplitAlign;
@@ -412,6 +420,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
       }
     }
     hipError_t err = p->dtype == PGSR_F32    ? launch_attn_f32(a, st)
+                     : pipe                  ? launch_attn_bf16_pipe(a, st)
                      : p->dtype == PGSR_BF16 ? launch_attn_bf16(a, st)
                                              : launch_attn_fp8(a, st);
     if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine(a, p->dtype == PGSR_F32, st);
@@ -561,6 +570,14 @@ int pgsr_pool_enable_timing(pgsr_pool* p, int on) {
   }
   p->timing = on != 0;
   p->timed_call = false;
+  return ok();
+}
+
+int pgsr_pool_set_prefill_kernel(pgsr_pool* p, int kind) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  if (kind != PGSR_PREFILL_AUTO && kind != PGSR_PREFILL_FOUR_WAVE)
+    return fail(PGSR_EINVAL, "unknown prefill kernel %d", kind);
+  p->prefill_kind = kind;
   return ok();
 }
 

@@ -99,6 +99,11 @@ class KVPool:
         vs = (ctypes.c_float * self.n_layers)(*map(float, v_scales))
         N.check(N.lib.pgsr_pool_set_kv_scales(self._h, ks, vs))
 
+    def set_prefill_kernel(self, kind: str) -> None:
+        """bf16 prefill kernel: "auto" (pipelined where it applies) or "four_wave"."""
+        code = {"auto": 0, "four_wave": 1}[kind]
+        N.check(N.lib.pgsr_pool_set_prefill_kernel(self._h, code))
+
     # ---- kernel timing (HIP events recorded by the library on the call's stream) ----
     def enable_timing(self, on: bool = True) -> None:
         N.check(N.lib.pgsr_pool_enable_timing(self._h, 1 if on else 0))

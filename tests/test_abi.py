@@ -79,3 +79,7 @@ def test_null_pool_and_gemm_validation(native):
     assert native.lib.pgsr_gemm_bf16(4, 12, 16, None, None, None, None, None) == native.EUNSUPPORTED
     assert native.lib.pgsr_gemm_bf16(0, 16, 16, None, None, None, None, None) == native.OK
     assert native.lib.pgsr_gemm_bf16(4, 16, 16, None, None, None, None, None) == native.EINVAL
+
+
+def test_prefill_kernel_choice_is_validated(native):
+    assert native.lib.pgsr_pool_set_prefill_kernel(None, 0) == native.EINVAL

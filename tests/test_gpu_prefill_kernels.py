@@ -1,0 +1,94 @@
+"""The software-pipelined bf16 prefill kernel (head_dim 128, GQA groups
+dividing 32) against the four-wave kernel and the fp64 oracle.  Both kernels
+take every query row through the same sequence of operations, so their outputs
+must agree bit for bit; each must also meet the bf16 tolerance against the
+oracle.  Cases cover every group size the pipelined kernel takes, block sizes
+16 / 32 / 64, crops not aligned to a block with NaN-poisoned tail slots,
+suffixes shorter than one query tile, tiles that straddle the diagonal, and
+several sequences of different lengths in one call."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from gpu_helpers import assert_close, contaminated_then_crop, dev, log, make_pool, oracle_suffix
+
+pytestmark = pytest.mark.gpu
+
+
+def _blocks(n, B):
+    return -(-n // B)
+
+
+def _run(kind, geom, eps, B, scale):
+    """Contaminated prefill, poisoned crop, then one replay call over all
+    episodes; returns the per-episode outputs."""
+    nb = sum(_blocks(e.t_contaminated, B) + _blocks(e.t_sanitized, B) for e in eps) + 4
+    mbps = max(_blocks(max(e.t_contaminated, e.t_sanitized), B) for e in eps) + 2
+    pool = make_pool(geom, "bf16", nb, len(eps), mbps, block_size=B)
+    pool.set_prefill_kernel(kind)
+    for i, e in enumerate(eps):
+        contaminated_then_crop(pool, e, i, scale, poison=True)
+    q, k, v = (torch.cat([dev(getattr(e, x)[e.prefix:], "bf16") for e in eps]) for x in ("q", "k", "v"))
+    o = torch.empty_like(q)
+    assert pool.replay(0, list(range(len(eps))), [e.suffix for e in eps], q, k, v, o, scale) == 0
+    torch.cuda.synchronize()
+    out, off = [], 0
+    for e in eps:
+        out.append(o[off:off + e.suffix])
+        off += e.suffix
+    return out
+
+
+CASES = [
+    # (Hq, Hkv, B, [(P, S), ...])
+    (32, 8, 16, [(300, 77)]),
+    (32, 8, 16, [(0, 130)]),
+    (32, 8, 16, [(8189, 96)]),          # the 8B crop point, short suffix
+    (32, 8, 16, [(64, 64)]),            # aligned prefix, one query tile
+    (32, 32, 16, [(100, 200)]),         # G = 1
+    (64, 2, 32, [(50, 70)]),            # G = 32
+    (16, 8, 64, [(129, 64)]),           # G = 2, B = 64
+    (32, 4, 32, [(1021, 3)]),           # G = 8, fewer queries than one 32-row block
+    (64, 4, 16, [(700, 45)]),           # G = 16
+    (32, 8, 16, [(517, 90), (0, 33), (2000, 257), (63, 1)]),   # ragged batch in one call
+]
+
+
+@pytest.mark.parametrize("hq,hkv,B,ps", CASES)
+def test_pipelined_equals_four_wave_and_oracle(hq, hkv, B, ps):
+    geom = W.AttnGeometry(hq, hkv, 128)
+    log(f"prefill kernels {hq}/{hkv} B={B} episodes {ps}")
+    rng = np.random.default_rng(hq * 7919 + B + sum(p for p, _ in ps))
+    eps = [W.draw_episode(rng, geom, "bf16", P, S, P + S + 3) for P, S in ps]
+    scale = 128 ** -0.5
+    pipe = _run("auto", geom, eps, B, scale)
+    four = _run("four_wave", geom, eps, B, scale)
+    for e, a, b in zip(eps, pipe, four):
+        assert torch.equal(a, b), f"pipelined and four-wave kernels differ (P={e.prefix}, S={e.suffix})"
+        assert_close(a.float().cpu().numpy(), oracle_suffix(e, scale), "bf16", f"P={e.prefix} S={e.suffix}")
+
+
+def test_pipelined_full_reset_equals_replay_at_8b_crop():
+    """Theorem 1 on the pipelined kernel at the unaligned 8B crop (P = 8189),
+    with a suffix spanning several query tiles."""
+    geom = W.AttnGeometry(32, 8, 128)
+    rng = np.random.default_rng(8189)
+    P, S = 8189, 640
+    ep = W.draw_episode(rng, geom, "bf16", P, S, P + S + 3)
+    scale = 128 ** -0.5
+    B = 16
+    pool = make_pool(geom, "bf16", 2 * _blocks(P + S + 3, B) + 4, 2, _blocks(P + S + 3, B) + 2)
+    contaminated_then_crop(pool, ep, 0, scale, poison=True)
+    q, k, v = (dev(getattr(ep, x)[P:], "bf16") for x in ("q", "k", "v"))
+    o = torch.empty_like(q)
+    assert pool.replay(0, [0], [S], q, k, v, o, scale) == 0
+    fq, fk, fv = (dev(getattr(ep, x), "bf16") for x in ("q", "k", "v"))
+    fo = torch.empty_like(fq)
+    assert pool.full_reset(0, [1], [P + S], fq, fk, fv, fo, scale) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(fo[P:], o)
+    rows = np.arange(0, S * 32, 37 * 32 + 5)         # flat (token, head) rows
+    ref = oracle_suffix(ep, scale, rows=rows)
+    got = o.reshape(S * 32, 128)[torch.from_numpy(rows).cuda()]
+    assert_close(got.float().cpu().numpy(), ref, "bf16", "8B crop, sampled rows")
