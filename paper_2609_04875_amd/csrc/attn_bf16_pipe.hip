@@ -150,15 +150,24 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   // lane index.
   int idv = 0;
   auto fetch_ids = [&](int kt) { idv = row[min(kt * KB + (lane < KB ? lane : 0), last_blk)]; };
+  // Per-lane element offsets of a thread's chunks inside a block-head (K:
+  // slot-major rows of D; V: d-major rows of B slots), fixed for the kernel;
+  // a load is then a scalar block pointer plus this offset.
+  int koff[CPT], voff[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int in = chunk_in(i);
+    koff[i] = (in / (D / 8)) * D + (in % (D / 8)) * 8;
+    voff[i] = (in / (B / 8)) * B + (in % (B / 8)) * 8;
+  }
   u32x4 kreg[CPT], vreg[CPT];
   auto load_tile = [&](int ids) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int in = chunk_in(i);
       const int id = __builtin_amdgcn_readlane(ids, chunk_blk(i));
       const int64_t base = (head_base + (int64_t)id * hkv) * (B * D);
-      kreg[i] = *(const u32x4*)(kc + base + (in / (D / 8)) * D + (in % (D / 8)) * 8);
-      vreg[i] = *(const u32x4*)(vc + base + (in / (B / 8)) * B + (in % (B / 8)) * 8);
+      kreg[i] = *(const u32x4*)((kc + base) + koff[i]);
+      vreg[i] = *(const u32x4*)((vc + base) + voff[i]);
     }
   };
   auto store_tile = [&](int buf, int kb) {
@@ -343,7 +352,13 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
     float mx[QB];
     row_max(sn, mx);
 #pragma unroll
-    for (int b = 0; b < QB; ++b) l[b] = fmaf(l[b], alpha[b], ps0[b] + ps1[b]);
+    for (int b = 0; b < QB; ++b) {
+      l[b] = fmaf(l[b], alpha[b], ps0[b] + ps1[b]);
+      // Keep this step's row sum in this step: otherwise the compiler sinks
+      // the dot products of both unrolled steps to the loop's end, where they
+      // run with no products to overlap and hold P live across a step.
+      asm volatile("" ::"v"(l[b]));
+    }
     commit_next(t);
     apply_max(mx);
   };
@@ -466,29 +481,23 @@ bool attn_bf16_pipe_eligible(int head_dim, int group) {
 
 int attn_bf16_pipe_tile_tokens(int group) { return kPW * kPQB * (32 / group); }
 
-hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s) {
-  if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
+hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
+  if (a.n <= 0 || a.n_tiles <= 0) {
+    record_idle(ev, s);
+    return hipSuccess;
+  }
   const int group = a.n_q_heads / a.n_kv_heads;
   if (!attn_bf16_pipe_eligible(a.head_dim, group)) return hipErrorInvalidValue;
-  dim3 grid(a.n_tiles * a.n_kv_heads * a.n_splits);
+  const dim3 grid(a.n_tiles * a.n_kv_heads * a.n_splits), blk(kPW * 64);
+  const auto* q = (const uint16_t*)a.q;
+  const auto* kc = (const uint16_t*)a.k_cache;
+  const auto* vc = (const uint16_t*)a.v_cache;
+  auto* o = (uint16_t*)a.o;
   switch (a.block_size) {
-    case 16:
-      hipLaunchKernelGGL(attn_bf16_pipe_kernel<16>, grid, dim3(kPW * 64), 0, s, a, a.tables,
-                         (const uint16_t*)a.q, (const uint16_t*)a.k_cache, (const uint16_t*)a.v_cache,
-                         (uint16_t*)a.o);
-      break;
-    case 32:
-      hipLaunchKernelGGL(attn_bf16_pipe_kernel<32>, grid, dim3(kPW * 64), 0, s, a, a.tables,
-                         (const uint16_t*)a.q, (const uint16_t*)a.k_cache, (const uint16_t*)a.v_cache,
-                         (uint16_t*)a.o);
-      break;
-    case 64:
-      hipLaunchKernelGGL(attn_bf16_pipe_kernel<64>, grid, dim3(kPW * 64), 0, s, a, a.tables,
-                         (const uint16_t*)a.q, (const uint16_t*)a.k_cache, (const uint16_t*)a.v_cache,
-                         (uint16_t*)a.o);
-      break;
-    default:
-      return hipErrorInvalidValue;
+    case 16: launch_kernel(attn_bf16_pipe_kernel<16>, grid, blk, s, ev.start, ev.stop, a, a.tables, q, kc, vc, o); break;
+    case 32: launch_kernel(attn_bf16_pipe_kernel<32>, grid, blk, s, ev.start, ev.stop, a, a.tables, q, kc, vc, o); break;
+    case 64: launch_kernel(attn_bf16_pipe_kernel<64>, grid, blk, s, ev.start, ev.stop, a, a.tables, q, kc, vc, o); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

@@ -194,7 +194,9 @@ __device__ inline uint8_t to_cache<uint16_t, uint8_t>(uint16_t x, float scale) {
 //   V: token p -> v_cache[layer][id][h][:][p % B]      (transposed via LDS)
 template <typename TI, typename T>
 __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
-  __shared__ T vstage[64 * 128];  // [slot][d], block_size <= 64, head_dim <= 128
+  // [slot][d] staging of V, rows padded by 8 elements on the 16-byte path
+  // (block_size <= 64, head_dim <= 128)
+  __shared__ __attribute__((aligned(16))) T vstage[64 * (128 + 8)];
   const int item = blockIdx.x;
   int ei = 0;
   while (ei + 1 < a.n && a.e[ei + 1].item_start <= item) ++ei;
@@ -226,6 +228,34 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
   const TI* vin = (const TI*)a.v_in;
   T* kc = (T*)a.k_cache + blk * B * D;
   T* vc = (T*)a.v_cache + blk * D * B;
+  if constexpr (sizeof(TI) == 2 && sizeof(T) == 2) {
+    // bf16 pool, span starting and ending on 8-slot boundaries: K rows move in
+    // 16-byte chunks; V is staged [slot][d] (rows padded to D + 8, so the
+    // transposing reads of 8 slots at one d fall in distinct banks) and each
+    // d row's 8-slot runs are written as 16-byte chunks.
+    if ((s0 & 7) == 0 && (nt & 7) == 0 && (D & 7) == 0) {
+      typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+      const int C8 = D / 8, DP = D + 8, S8 = nt / 8;
+      const int64_t row_stride = (int64_t)a.n_kv_heads * D;
+      const int64_t src0 = ((int64_t)(e.q_off + (p0 - e.prefix)) * a.n_kv_heads + h) * D;
+      for (int i = threadIdx.x; i < nt * C8; i += blockDim.x) {
+        const int t = i / C8, c = (i % C8) * 8;
+        const int64_t src = src0 + t * row_stride + c;
+        *(u4*)(kc + (int64_t)(s0 + t) * D + c) = *(const u4*)((const TI*)a.k_in + src);
+        *(u4*)(&vstage[t * DP + c]) = *(const u4*)((const TI*)a.v_in + src);
+      }
+      __syncthreads();
+      for (int i = threadIdx.x; i < D * S8; i += blockDim.x) {
+        const int d = i / S8, t0 = (i % S8) * 8;
+        u4 out;
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          out[w] = (uint32_t)vstage[(t0 + 2 * w) * DP + d] | ((uint32_t)vstage[(t0 + 2 * w + 1) * DP + d] << 16);
+        *(u4*)(vc + (int64_t)d * B + s0 + t0) = out;
+      }
+      return;
+    }
+  }
   for (int i = threadIdx.x; i < nt * D; i += blockDim.x) {
     const int t = i / D, c = i % D;
     const int64_t src = ((int64_t)(e.q_off + (p0 - e.prefix) + t) * a.n_kv_heads + h) * D + c;
@@ -278,20 +308,24 @@ hipError_t launch_poison(const PoisonArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s) {
-  if (a.n <= 0 || a.n_items <= 0) return hipSuccess;
+hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s, const LaunchEvents& ev) {
+  if (a.n <= 0 || a.n_items <= 0) {
+    record_idle(ev, s);
+    return hipSuccess;
+  }
   bool any_cow = false;
   for (int i = 0; i < a.n; ++i) any_cow |= a.e[i].cow_old >= 0;
-  const dim3 cow_grid(a.n, a.n_kv_heads), grid(a.n_items, a.n_kv_heads);
+  const dim3 cow_grid(a.n, a.n_kv_heads), grid(a.n_items, a.n_kv_heads), blk(256);
+  hipEvent_t first = any_cow ? nullptr : ev.start;    // the append kernel's start event
   if (elem_bytes == 4) {
-    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint32_t>, cow_grid, dim3(256), 0, s, a);
-    hipLaunchKernelGGL((append_kernel<uint32_t, uint32_t>), grid, dim3(256), 0, s, a);
+    if (any_cow) launch_kernel(cow_kernel<uint32_t>, cow_grid, blk, s, ev.start, nullptr, a);
+    launch_kernel(append_kernel<uint32_t, uint32_t>, grid, blk, s, first, ev.stop, a);
   } else if (elem_bytes == 2) {
-    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint16_t>, cow_grid, dim3(256), 0, s, a);
-    hipLaunchKernelGGL((append_kernel<uint16_t, uint16_t>), grid, dim3(256), 0, s, a);
+    if (any_cow) launch_kernel(cow_kernel<uint16_t>, cow_grid, blk, s, ev.start, nullptr, a);
+    launch_kernel(append_kernel<uint16_t, uint16_t>, grid, blk, s, first, ev.stop, a);
   } else {                                          // FP8 cache, bf16 inputs
-    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint8_t>, cow_grid, dim3(256), 0, s, a);
-    hipLaunchKernelGGL((append_kernel<uint16_t, uint8_t>), grid, dim3(256), 0, s, a);
+    if (any_cow) launch_kernel(cow_kernel<uint8_t>, cow_grid, blk, s, ev.start, nullptr, a);
+    launch_kernel(append_kernel<uint16_t, uint8_t>, grid, blk, s, first, ev.stop, a);
   }
   return hipGetLastError();
 }

@@ -20,9 +20,14 @@ _DT = {N.F32: (torch.float32, torch.float32), N.BF16: (torch.bfloat16, torch.bfl
        N.FP8_E4M3: (torch.uint8, torch.bfloat16)}
 
 
-def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> Optional[int]:
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return s.cuda_stream or None
+def _stream_ptr(stream: Optional[torch.cuda.Stream], device: Optional[int] = None) -> Optional[int]:
+    """Raw HIP stream handle: the given stream, else torch's current stream on
+    ``device`` (read without building a Stream object, which costs several
+    microseconds per call)."""
+    if stream is not None:
+        return stream.cuda_stream or None
+    idx = torch.cuda.current_device() if device is None else device
+    return torch._C._cuda_getCurrentRawStream(idx) or None
 
 
 def _dev_ptr(t: Optional[torch.Tensor], dtype, name: str) -> Optional[int]:
@@ -64,6 +69,7 @@ class KVPool:
             self.workspace.data_ptr() if self.workspace is not None else None,
             workspace_bytes, order, _stream_ptr(stream), ctypes.byref(handle)))
         self._h = handle
+        self._dev = self.k_cache.device.index
         self.recomputed_tokens = ctypes.c_int64(0)
 
     def close(self) -> None:
@@ -89,7 +95,7 @@ class KVPool:
         return out.value
 
     def refresh(self, stream=None) -> None:
-        N.check(N.lib.pgsr_pool_refresh(self._h, _stream_ptr(stream)))
+        N.check(N.lib.pgsr_pool_refresh(self._h, _stream_ptr(stream, self._dev)))
 
     def set_kv_scales(self, k_scales: Sequence[float], v_scales: Sequence[float]) -> None:
         """Per-layer K and V scales of an FP8 pool (stored code = x / scale)."""
@@ -119,19 +125,19 @@ class KVPool:
              stream=None) -> int:
         """Restore = crop; returns the status (0 ok) instead of raising."""
         return N.lib.pgsr_kv_crop(self._h, len(seqs), N.int32_array(seqs), N.int32_array(new_lens),
-                                  N.POISON if poison else 0, _stream_ptr(stream))
+                                  N.POISON if poison else 0, _stream_ptr(stream, self._dev))
 
     def fork(self, srcs: Sequence[int], dsts: Sequence[int], stream=None) -> int:
         """Copy-on-write fork of srcs[i] into the empty dsts[i]; returns the status."""
         return N.lib.pgsr_kv_fork(self._h, len(srcs), N.int32_array(srcs), N.int32_array(dsts),
-                                  _stream_ptr(stream))
+                                  _stream_ptr(stream, self._dev))
 
     def _prefill(self, fn, layer, seqs, q_lens, q, k, v, o, scale, commit, stream) -> int:
         dt = self.dtype
         return fn(self._h, layer, len(seqs), N.int32_array(seqs), N.int32_array(q_lens),
                   _dev_ptr(q, dt, "q"), _dev_ptr(k, dt, "k"), _dev_ptr(v, dt, "v"),
                   _dev_ptr(o, dt, "o"), float(scale), N.COMMIT if commit else 0,
-                  ctypes.byref(self.recomputed_tokens), _stream_ptr(stream))
+                  ctypes.byref(self.recomputed_tokens), _stream_ptr(stream, self._dev))
 
     def replay(self, layer: int, seqs, q_lens, q, k, v, o, scale: float, commit: bool = True,
                stream=None) -> int:
