@@ -32,11 +32,13 @@
 //     the PV product (v_dot2_f32_bf16 against ones).
 //   * O^T += V^T P^T with the same MFMA (A = V^T rows from LDS, B = P^T taken
 //     straight from the S^T registers after rounding to bf16).  The reduction
-//     index of a B operand must match the A operand's, and a lane's S^T
-//     registers hold keys {4h..4h+3, 8+4h..8+4h+3} of each 16-key group (h =
-//     lane half); V^T is therefore stored in LDS with the 4-key chunks of every
-//     16-key group in the order [0, 2, 1, 3], which makes those 8 keys one
-//     contiguous 16-byte LDS read.
+//     index of a B operand must match the A operand's.  In the 32x32
+//     accumulator, lane half h holds rows {8a + 4h + c} (a = 0..3, c = 0..3);
+//     the K operand therefore reads, for accumulator row i, key pi(i), where pi
+//     swaps bits 2 and 3 of i.  Then lane half h holds keys 8h..8h+7 of each
+//     16-key group in order, and the matching V^T operand is 8 consecutive keys
+//     of one d row: V^T sits in LDS in natural key order and every operand is
+//     one 16-byte read.
 // LDS rows are padded by 16 bytes (K: D+8 elements, V^T: 72), which spreads
 // the 32 rows one MFMA operand read touches over distinct bank groups and keeps
 // every operand address a base plus an immediate offset.
@@ -201,10 +203,7 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
         if (pos0 >= kv_len) val = u32x4{0, 0, 0, 0};
         else if (pos0 + 8 > kv_len) val = zero_tail(val, pos0, kv_len);
       }
-      const int base = dd * VLD + (key0 & ~15);
-      const int half = (key0 >> 3) & 1;          // 4-key chunks 2h, 2h+1 -> slots h, h+2
-      *(u32x2*)&v_lds[buf][base + 4 * half] = u32x2{val[0], val[1]};
-      *(u32x2*)&v_lds[buf][base + 4 * half + 8] = u32x2{val[2], val[3]};
+      *(u32x4*)&v_lds[buf][dd * VLD + key0] = val;
     }
   };
 
@@ -218,7 +217,8 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   auto qk = [&](int buf, f32x16 (&s)[2]) {
     s[0] = f32x16{};
     s[1] = f32x16{};
-    const uint16_t* kp = &k_lds[buf][r * KLD + 8 * hh];
+    const int kr = (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);   // pi(r): bits 2 and 3 swapped
+    const uint16_t* kp = &k_lds[buf][kr * KLD + 8 * hh];
     constexpr int N = D / 16;
     bf16x8 k0[N], k1[N];
 #pragma unroll
@@ -297,7 +297,7 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int key = kb + kh * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+          const int key = kb + kh * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
           s[kh][i] = key > qpos ? -INFINITY : s[kh][i];
         }
     }

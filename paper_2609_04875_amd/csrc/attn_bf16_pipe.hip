@@ -17,9 +17,10 @@
 //   so row max and row sum are in-lane plus one exchange between lane halves.
 //   Online softmax in base 2 with a lazy rescale (the running max moves only
 //   when a tile exceeds it by more than 2^8); P is rounded to bf16 and the row
-//   sum adds exactly those values; O^T += V^T P^T with V^T stored in LDS with
-//   the 4-key chunks of each 16-key group in the order [0, 2, 1, 3], matching
-//   the keys a lane's S^T registers hold.
+//   sum adds exactly those values; O^T += V^T P^T.  Accumulator row i of S^T
+//   is key pi(i) (bits 2 and 3 of i swapped), so a lane's P^T registers hold
+//   8 consecutive keys of each 16-key group and V^T sits in LDS in natural
+//   key order: every operand is one 16-byte read.
 //
 // Pipeline.  Tiles whose keys all precede the workgroup's first query need no
 // causal mask.  For those, step t issues the products S(t+1) = K(t+1) Q^T
@@ -179,10 +180,7 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       const int dd = in / (B / 8), key0 = blk * B + (in % (B / 8)) * 8;
       u32x4 val = vreg[i];
       if (tail) val = zero_tail(val, kb + key0, kv_len);   // selects only: no per-lane branch
-      const int base = dd * VLD + (key0 & ~15);
-      const int half = (key0 >> 3) & 1;
-      *(u32x2*)&v_lds[buf][base + 4 * half] = u32x2{val[0], val[1]};
-      *(u32x2*)&v_lds[buf][base + 4 * half + 8] = u32x2{val[2], val[3]};
+      *(u32x4*)&v_lds[buf][dd * VLD + key0] = val;
     }
   };
   // One pipeline step's memory work around its compute: gather tile x+2 at
@@ -212,8 +210,9 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
     m_use[b] = 0.f;
   }
 
+  const int kr = (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);   // pi(r): bits 2 and 3 swapped
   auto k_op = [&](int buf, int kh, int ds) {
-    return __builtin_bit_cast(bf16x8, *(const u32x4*)&k_lds[buf][(kh * 32 + r) * KLD + 16 * ds + 8 * hh]);
+    return __builtin_bit_cast(bf16x8, *(const u32x4*)&k_lds[buf][(kh * 32 + kr) * KLD + 16 * ds + 8 * hh]);
   };
   auto v_op = [&](int buf, int ks, int db) {
     return __builtin_bit_cast(bf16x8, *(const u32x4*)&v_lds[buf][(db * 32 + r) * VLD + ks * 16 + 8 * hh]);
@@ -417,7 +416,7 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int key = kb + kh * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+          const int key = kb + kh * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
           sa[b][kh][i] = key > qpos[b] ? -INFINITY : sa[b][kh][i];
         }
     update_max(sa);
