@@ -439,61 +439,53 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, TO* __re
 int attn_bf16_tile_tokens(int, int group) { return kNW * (32 / group); }
 
 template <int D, int B, bool F8>
-static void launch_d_b(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
+static void launch_d_b(const AttnArgs& a, hipStream_t s) {
   using CT = std::conditional_t<F8, uint8_t, uint16_t>;
   dim3 grid(a.n_tiles * a.n_kv_heads * a.n_splits);
-  launch_kernel(attn_bf16_kernel<D, kNW, B, F8>, grid, dim3(kNW * 64), s, ev.start, ev.stop, a, a.tables,
-                (const uint16_t*)a.q, (const CT*)a.k_cache, (const CT*)a.v_cache, (uint16_t*)a.o);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, kNW, B, F8>), grid, dim3(kNW * 64), 0, s, a, a.tables,
+                     (const uint16_t*)a.q, (const CT*)a.k_cache, (const CT*)a.v_cache,
+                     (uint16_t*)a.o);
 }
 
 template <int D, bool F8>
-static hipError_t launch_d(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
+static hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
   switch (a.block_size) {
-    case 16: launch_d_b<D, 16, F8>(a, s, ev); break;
-    case 32: launch_d_b<D, 32, F8>(a, s, ev); break;
-    case 64: launch_d_b<D, 64, F8>(a, s, ev); break;
+    case 16: launch_d_b<D, 16, F8>(a, s); break;
+    case 32: launch_d_b<D, 32, F8>(a, s); break;
+    case 64: launch_d_b<D, 64, F8>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s, const LaunchEvents& ev) {
-  if (a.n_rows <= 0) {
-    record_idle(ev, s);
-    return hipSuccess;
-  }
+hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s) {
+  if (a.n_rows <= 0) return hipSuccess;
   const int rows_per_block = 256 / (a.head_dim / 8);
-  dim3 grid((a.n_rows + rows_per_block - 1) / rows_per_block), blk(256);
+  dim3 grid((a.n_rows + rows_per_block - 1) / rows_per_block);
   if (a.head_dim == 128 && f32_out)
-    launch_kernel(split_combine_kernel<128, float>, grid, blk, s, ev.start, ev.stop, a, (float*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<128, float>), grid, dim3(256), 0, s, a, (float*)a.o);
   else if (a.head_dim == 64 && f32_out)
-    launch_kernel(split_combine_kernel<64, float>, grid, blk, s, ev.start, ev.stop, a, (float*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<64, float>), grid, dim3(256), 0, s, a, (float*)a.o);
   else if (a.head_dim == 128)
-    launch_kernel(split_combine_kernel<128, uint16_t>, grid, blk, s, ev.start, ev.stop, a, (uint16_t*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<128, uint16_t>), grid, dim3(256), 0, s, a, (uint16_t*)a.o);
   else if (a.head_dim == 64)
-    launch_kernel(split_combine_kernel<64, uint16_t>, grid, blk, s, ev.start, ev.stop, a, (uint16_t*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<64, uint16_t>), grid, dim3(256), 0, s, a, (uint16_t*)a.o);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
-  if (a.n <= 0 || a.n_tiles <= 0) {
-    record_idle(ev, s);
-    return hipSuccess;
-  }
-  if (a.head_dim == 128) return launch_d<128, false>(a, s, ev);
-  if (a.head_dim == 64) return launch_d<64, false>(a, s, ev);
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
+  if (a.head_dim == 128) return launch_d<128, false>(a, s);
+  if (a.head_dim == 64) return launch_d<64, false>(a, s);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
-  if (a.n <= 0 || a.n_tiles <= 0) {
-    record_idle(ev, s);
-    return hipSuccess;
-  }
-  if (a.head_dim == 128) return launch_d<128, true>(a, s, ev);
-  if (a.head_dim == 64) return launch_d<64, true>(a, s, ev);
+hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s) {
+  if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
+  if (a.head_dim == 128) return launch_d<128, true>(a, s);
+  if (a.head_dim == 64) return launch_d<64, true>(a, s);
   return hipErrorInvalidValue;
 }
 

@@ -480,11 +480,8 @@ bool attn_bf16_pipe_eligible(int head_dim, int group) {
 
 int attn_bf16_pipe_tile_tokens(int group) { return kPW * kPQB * (32 / group); }
 
-hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
-  if (a.n <= 0 || a.n_tiles <= 0) {
-    record_idle(ev, s);
-    return hipSuccess;
-  }
+hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s) {
+  if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
   const int group = a.n_q_heads / a.n_kv_heads;
   if (!attn_bf16_pipe_eligible(a.head_dim, group)) return hipErrorInvalidValue;
   const dim3 grid(a.n_tiles * a.n_kv_heads * a.n_splits), blk(kPW * 64);
@@ -493,9 +490,9 @@ hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s, const LaunchE
   const auto* vc = (const uint16_t*)a.v_cache;
   auto* o = (uint16_t*)a.o;
   switch (a.block_size) {
-    case 16: launch_kernel(attn_bf16_pipe_kernel<16>, grid, blk, s, ev.start, ev.stop, a, a.tables, q, kc, vc, o); break;
-    case 32: launch_kernel(attn_bf16_pipe_kernel<32>, grid, blk, s, ev.start, ev.stop, a, a.tables, q, kc, vc, o); break;
-    case 64: launch_kernel(attn_bf16_pipe_kernel<64>, grid, blk, s, ev.start, ev.stop, a, a.tables, q, kc, vc, o); break;
+    case 16: hipLaunchKernelGGL(attn_bf16_pipe_kernel<16>, grid, blk, 0, s, a, a.tables, q, kc, vc, o); break;
+    case 32: hipLaunchKernelGGL(attn_bf16_pipe_kernel<32>, grid, blk, 0, s, a, a.tables, q, kc, vc, o); break;
+    case 64: hipLaunchKernelGGL(attn_bf16_pipe_kernel<64>, grid, blk, 0, s, a, a.tables, q, kc, vc, o); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

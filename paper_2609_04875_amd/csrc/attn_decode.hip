@@ -265,20 +265,20 @@ attn_decode_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_
 }
 
 template <int D, int B, bool F8>
-void launch_dec(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
+void launch_dec(const AttnArgs& a, hipStream_t s) {
   using CT = std::conditional_t<F8, uint8_t, uint16_t>;
   const int64_t waves = (int64_t)a.n * a.n_kv_heads * a.n_splits;
-  launch_kernel(attn_decode_kernel<D, B, F8>, dim3((unsigned)((waves + 3) / 4)), dim3(256), s, ev.start,
-                ev.stop, a, a.tables, (const uint16_t*)a.q, (const CT*)a.k_cache, (const CT*)a.v_cache,
-                (uint16_t*)a.o);
+  hipLaunchKernelGGL((attn_decode_kernel<D, B, F8>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a,
+                     a.tables, (const uint16_t*)a.q, (const CT*)a.k_cache, (const CT*)a.v_cache,
+                     (uint16_t*)a.o);
 }
 
 template <int D, bool F8>
-hipError_t launch_dec_d(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
+hipError_t launch_dec_d(const AttnArgs& a, hipStream_t s) {
   switch (a.block_size) {
-    case 16: launch_dec<D, 16, F8>(a, s, ev); break;
-    case 32: launch_dec<D, 32, F8>(a, s, ev); break;
-    case 64: launch_dec<D, 64, F8>(a, s, ev); break;
+    case 16: launch_dec<D, 16, F8>(a, s); break;
+    case 32: launch_dec<D, 32, F8>(a, s); break;
+    case 64: launch_dec<D, 64, F8>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -288,13 +288,10 @@ hipError_t launch_dec_d(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev
 
 int attn_decode_keys_per_tile() { return kDecKT; }
 
-hipError_t launch_attn_decode(const AttnArgs& a, bool fp8, hipStream_t s, const LaunchEvents& ev) {
-  if (a.n <= 0) {
-    record_idle(ev, s);
-    return hipSuccess;
-  }
-  if (a.head_dim == 128) return fp8 ? launch_dec_d<128, true>(a, s, ev) : launch_dec_d<128, false>(a, s, ev);
-  if (a.head_dim == 64) return fp8 ? launch_dec_d<64, true>(a, s, ev) : launch_dec_d<64, false>(a, s, ev);
+hipError_t launch_attn_decode(const AttnArgs& a, bool fp8, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  if (a.head_dim == 128) return fp8 ? launch_dec_d<128, true>(a, s) : launch_dec_d<128, false>(a, s);
+  if (a.head_dim == 64) return fp8 ? launch_dec_d<64, true>(a, s) : launch_dec_d<64, false>(a, s);
   return hipErrorInvalidValue;
 }
 

@@ -205,16 +205,13 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
 
 int attn_f32_tile_tokens(int, int) { return kTokens; }
 
-hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev) {
-  if (a.n <= 0 || a.n_tiles <= 0) {
-    record_idle(ev, s);
-    return hipSuccess;
-  }
+hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s) {
+  if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
   dim3 grid(a.n_tiles * a.n_splits, a.n_q_heads);
   if (a.head_dim == 64)
-    launch_kernel(attn_f32_kernel<64, 32>, grid, dim3(kWaves * 64), s, ev.start, ev.stop, a);
+    hipLaunchKernelGGL((attn_f32_kernel<64, 32>), grid, dim3(kWaves * 64), 0, s, a);
   else if (a.head_dim == 128)
-    launch_kernel(attn_f32_kernel<128, 16>, grid, dim3(kWaves * 64), s, ev.start, ev.stop, a);
+    hipLaunchKernelGGL((attn_f32_kernel<128, 16>), grid, dim3(kWaves * 64), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

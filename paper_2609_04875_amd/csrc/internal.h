@@ -4,7 +4,6 @@
 // several launches of at most kMaxSeqsPerLaunch sequences each.
 #pragma once
 
-#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -13,28 +12,6 @@
 namespace pgsr {
 
 constexpr int kMaxSeqsPerLaunch = 64;
-
-// Events a launch function attaches to its kernels' own dispatches: start when
-// its first kernel begins, stop when its last kernel ends.  The events then
-// time the kernels themselves, with no marker packets between launches.
-struct LaunchEvents {
-  hipEvent_t start = nullptr, stop = nullptr;
-};
-
-template <typename... KArgs, typename... Args>
-inline void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s,
-                          hipEvent_t start, hipEvent_t stop, Args... args) {
-  if (start || stop)
-    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, start, stop, 0, args...);
-  else
-    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
-}
-
-// A launch function with no kernel to run still records its events.
-inline void record_idle(const LaunchEvents& ev, hipStream_t s) {
-  if (ev.start) (void)hipEventRecord(ev.start, s);
-  if (ev.stop) (void)hipEventRecord(ev.stop, s);
-}
 
 // ---------------------------------------------------------------- crop ---- //
 struct CropEntry {
@@ -186,26 +163,25 @@ int attn_bf16_tile_tokens(int head_dim, int group);
 hipError_t launch_crop(const CropArgs& a, hipStream_t s);
 hipError_t launch_poison(const PoisonArgs& a, hipStream_t s);
 hipError_t launch_fork(const ForkArgs& a, hipStream_t s);
-hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s, const LaunchEvents& ev = {});
-hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev = {});
-hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev = {});
+hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s);
+hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 // Software-pipelined bf16 prefill for head_dim 128 and GQA groups dividing
 // 32: one wave per SIMD, 64 query rows per wave, one workgroup per CU.
 bool attn_bf16_pipe_eligible(int head_dim, int group);
 int attn_bf16_pipe_tile_tokens(int group);
-hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev = {});
+hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s);
 // Same kernel over an FP8 E4M3 cache: codes widen to bf16 exactly on the way
 // into LDS; the K scale is in scale_log2, the V scale in o_scale.
-hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s, const LaunchEvents& ev = {});
+hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s);
 // Decode attention (every sequence of the launch has at most 32 / G query
 // tokens): one wave per (sequence, KV head, split) gathering MFMA operands from
 // the cache without LDS; with n_splits > 1 it writes split partials.
-hipError_t launch_attn_decode(const AttnArgs& a, bool fp8, hipStream_t s, const LaunchEvents& ev = {});
+hipError_t launch_attn_decode(const AttnArgs& a, bool fp8, hipStream_t s);
 int attn_decode_keys_per_tile();
 // Merge split-key partials into O (bf16, or fp32 for fp32 pools), splits in
 // increasing order.
-hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s,
-                                const LaunchEvents& ev = {});
+hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s);
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
                             int32_t* free_list, int32_t n_blocks, int32_t* free_top, int32_t* refs,
                             hipStream_t s);

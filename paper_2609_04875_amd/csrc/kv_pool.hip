@@ -308,24 +308,20 @@ hipError_t launch_poison(const PoisonArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s, const LaunchEvents& ev) {
-  if (a.n <= 0 || a.n_items <= 0) {
-    record_idle(ev, s);
-    return hipSuccess;
-  }
+hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s) {
+  if (a.n <= 0 || a.n_items <= 0) return hipSuccess;
   bool any_cow = false;
   for (int i = 0; i < a.n; ++i) any_cow |= a.e[i].cow_old >= 0;
-  const dim3 cow_grid(a.n, a.n_kv_heads), grid(a.n_items, a.n_kv_heads), blk(256);
-  hipEvent_t first = any_cow ? nullptr : ev.start;    // the append kernel's start event
+  const dim3 cow_grid(a.n, a.n_kv_heads), grid(a.n_items, a.n_kv_heads);
   if (elem_bytes == 4) {
-    if (any_cow) launch_kernel(cow_kernel<uint32_t>, cow_grid, blk, s, ev.start, nullptr, a);
-    launch_kernel(append_kernel<uint32_t, uint32_t>, grid, blk, s, first, ev.stop, a);
+    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint32_t>, cow_grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((append_kernel<uint32_t, uint32_t>), grid, dim3(256), 0, s, a);
   } else if (elem_bytes == 2) {
-    if (any_cow) launch_kernel(cow_kernel<uint16_t>, cow_grid, blk, s, ev.start, nullptr, a);
-    launch_kernel(append_kernel<uint16_t, uint16_t>, grid, blk, s, first, ev.stop, a);
+    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint16_t>, cow_grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((append_kernel<uint16_t, uint16_t>), grid, dim3(256), 0, s, a);
   } else {                                          // FP8 cache, bf16 inputs
-    if (any_cow) launch_kernel(cow_kernel<uint8_t>, cow_grid, blk, s, ev.start, nullptr, a);
-    launch_kernel(append_kernel<uint16_t, uint8_t>, grid, blk, s, first, ev.stop, a);
+    if (any_cow) hipLaunchKernelGGL(cow_kernel<uint8_t>, cow_grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((append_kernel<uint16_t, uint8_t>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

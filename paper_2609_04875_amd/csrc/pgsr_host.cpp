@@ -259,16 +259,10 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
   const bool commit = (flags & PGSR_COMMIT) != 0;
   const int eb = elem_bytes(p);
 
-  // Kernel timing: a call that fits one launch of each kernel attaches the
-  // events to those launches (they time the kernels themselves); larger calls
-  // bracket their launches with marker events.
-  const bool attached = p->timing && !segs.empty() && segs.size() <= (size_t)kMaxSeqsPerLaunch;
-  if (p->timing && !attached) {
+  if (p->timing) {
     hipError_t err = hipEventRecord(p->ev[0], st);
     if (err != hipSuccess) return hip_fail(err, "timing event");
   }
-  LaunchEvents append_ev;
-  if (attached) append_ev = {p->ev[0], p->ev[1]};
   // Reserve + append, chunked; the mirror takes the same pops in call order.
   for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
     const int32_t cnt = (int32_t)std::min<size_t>(kMaxSeqsPerLaunch, segs.size() - base);
@@ -326,11 +320,11 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.n_items = items;
     a.write_top = 1;
     a.top_after = p->h_top;
-    hipError_t err = launch_append(a, eb, st, append_ev);
+    hipError_t err = launch_append(a, eb, st);
     if (err != hipSuccess) return hip_fail(err, "append launch");
   }
 
-  if (p->timing && !attached) {
+  if (p->timing) {
     hipError_t err = hipEventRecord(p->ev[1], st);
     if (err == hipSuccess) err = hipEventRecord(p->ev[2], st);
     if (err != hipSuccess) return hip_fail(err, "timing event");
@@ -400,14 +394,8 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
         a.ws_acc = (float*)p->workspace;
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
-      const bool split = a.n_splits > 1;
-      LaunchEvents kev, cev;
-      if (attached) {
-        kev = {p->ev[2], split ? nullptr : p->ev[3]};
-        cev = {nullptr, p->ev[3]};
-      }
-      hipError_t err = launch_attn_decode(a, p->dtype == PGSR_FP8_E4M3, st, kev);
-      if (err == hipSuccess && split) err = launch_split_combine(a, false, st, cev);
+      hipError_t err = launch_attn_decode(a, p->dtype == PGSR_FP8_E4M3, st);
+      if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine(a, false, st);
       if (err != hipSuccess) return hip_fail(err, "decode attention launch");
       continue;
     }
@@ -431,25 +419,19 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
     }
-    const bool split = a.n_splits > 1;
-    LaunchEvents kev, cev;
-    if (attached) {
-      kev = {p->ev[2], split ? nullptr : p->ev[3]};
-      cev = {nullptr, p->ev[3]};
-    }
-    hipError_t err = p->dtype == PGSR_F32    ? launch_attn_f32(a, st, kev)
-                     : pipe                  ? launch_attn_bf16_pipe(a, st, kev)
-                     : p->dtype == PGSR_BF16 ? launch_attn_bf16(a, st, kev)
-                                             : launch_attn_fp8(a, st, kev);
-    if (err == hipSuccess && split) err = launch_split_combine(a, p->dtype == PGSR_F32, st, cev);
+    hipError_t err = p->dtype == PGSR_F32    ? launch_attn_f32(a, st)
+                     : pipe                  ? launch_attn_bf16_pipe(a, st)
+                     : p->dtype == PGSR_BF16 ? launch_attn_bf16(a, st)
+                                             : launch_attn_fp8(a, st);
+    if (err == hipSuccess && a.n_splits > 1) err = launch_split_combine(a, p->dtype == PGSR_F32, st);
     if (err != hipSuccess) return hip_fail(err, "attention launch");
   }
 
-  if (p->timing && !attached) {
+  if (p->timing) {
     hipError_t err = hipEventRecord(p->ev[3], st);
     if (err != hipSuccess) return hip_fail(err, "timing event");
+    p->timed_call = true;
   }
-  if (p->timing) p->timed_call = true;
   if (commit) {
     int64_t total = 0;
     for (int32_t i = 0; i < n; ++i) {
