@@ -222,7 +222,7 @@ int pgsr_pool_last_times(pgsr_pool *pool, float *append_ms, float *attention_ms)
 /*
  * Choice of the bf16 prefill attention kernel (Algorithm 1 replay loop,
  * prefill form).  PGSR_PREFILL_AUTO (the default) runs the software-pipelined
- * kernel (one wave per SIMD, 64 query rows per wave) wherever it applies:
+ * kernel (two waves per SIMD, 32 query rows per wave) wherever it applies:
  * head_dim 128, a GQA group dividing 32, a bf16 pool; every other call runs
  * the four-wave kernel.  PGSR_PREFILL_FOUR_WAVE runs the four-wave kernel for
  * every call.  Both give identical bits for every query row; the option only

@@ -2,14 +2,15 @@
 // cores (gfx950), software-pipelined so that each wave overlaps its own
 // matrix products with its own softmax arithmetic.
 //
-// Work decomposition.  A workgroup of 4 wave64s, one per SIMD (the whole
-// register file of a SIMD belongs to one wave), owns one KV head g and a tile
-// of 4 * 2 * 32 / G consecutive suffix tokens with the G query heads sharing g
-// (G divides 32).  Each wave owns 64 query rows (token, head) as two 32-row
-// blocks; every K or V^T operand a wave reads from LDS feeds one product per
-// block.  blockIdx.x = tile * n_kv_heads + g, so all tiles of a KV head land
-// on one XCD and share its L2 copy of the head's keys and values; tiles are
-// issued costliest first.
+// Work decomposition.  A workgroup of 8 wave64s, two per SIMD (each wave
+// holds up to 256 VGPRs), owns one KV head g and a tile of 8 * 32 / G
+// consecutive suffix tokens with the G query heads sharing g (G divides 32);
+// each wave owns one 32-row block of (token, head) query rows, and the two
+// waves of a SIMD interleave their matrix products with each other's softmax
+// arithmetic.  Three 35 KB LDS tile buffers keep one workgroup per CU.
+// blockIdx.x = tile * n_kv_heads + g, so all tiles of a KV head land on one
+// XCD and share its L2 copy of the head's keys and values; tiles are issued
+// costliest first.
 //
 // Per 64-key tile at absolute positions kb .. kb+63, in fp32:
 //   S^T = K Q^T (v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q^T in
