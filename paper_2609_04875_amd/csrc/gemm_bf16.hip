@@ -2,15 +2,21 @@
 // with W in the linear-layer layout [n][k]: fp32 accumulation on
 // v_mfma_f32_32x32x16_bf16 and one round-to-nearest-even store.
 //
-// A workgroup of 4 waves computes a 128 x 128 output tile, each wave a 64 x 64
-// quarter as 2 x 2 MFMA tiles.  K advances 64 at a time through padded,
-// double-buffered LDS tiles of X rows and W rows (both k-contiguous, so both
-// MFMA operands are 16-byte reads); the next K step is loaded into registers
-// while the current one is multiplied.  The product is formed transposed
-// (A = W rows, B = X rows): a lane then holds one output row and groups of 4
-// consecutive columns, stored as 8-byte writes.  The K loop never splits, so
-// each output element's accumulation order is fixed (rows of Y are bitwise
-// independent of which other rows share the launch).
+// A workgroup computes a BM x BN output tile with WGM x WGN waves, each wave a
+// (TM * 32) x (TN * 32) block as TM x TN MFMA tiles: 256 x 256 with 8 waves of
+// 2 x 4 tiles for large products (one workgroup per CU, 144 KB of LDS), and
+// 128 x 128 with 4 waves of 2 x 2 tiles when the large tile would leave CUs
+// idle.  K advances 64 at a time through padded, double-buffered LDS tiles of
+// X rows and W rows (both k-contiguous, so both MFMA operands are 16-byte
+// reads); the next K step is loaded into registers while the current one is
+// multiplied.  The product is formed transposed (A = W rows, B = X rows): a
+// lane then holds one output row and groups of 4 consecutive columns, stored
+// as 8-byte writes.  Output tiles are numbered so that each XCD (workgroup id
+// mod 8) takes a contiguous run of them, walked in groups of 8 tile rows, and
+// the workgroups sharing an XCD's L2 share their X and W panels.  The K loop
+// never splits and both tile shapes run the same products in the same order,
+// so each output element's accumulation order is fixed (rows of Y are
+// bitwise independent of which other rows share the launch).
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -26,109 +32,151 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int BM = 128, BN = 128, BK = 64;
+constexpr int BK = 64;
 constexpr int LDK = BK + 8;                      // LDS row stride (elements), 144 bytes
-constexpr int CPT = BM * BK / 8 / 256;           // 16-byte chunks per thread per operand
+constexpr int kGroupM = 8;                       // tile rows per group of the tile order
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-__global__ void __launch_bounds__(256, 2)
+template <int WGM, int WGN, int TM, int TN, int MINB>
+__global__ void __launch_bounds__(WGM * WGN * 64, MINB)
 gemm_bf16_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
                  const uint16_t* __restrict__ W, const uint16_t* R, uint16_t* Y) {
+  constexpr int NT = WGM * WGN * 64;
+  constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
+  constexpr int CPX = BM * BK / 8 / NT, CPW = BN * BK / 8 / NT;   // 16-byte chunks per thread
+  static_assert(CPX * NT * 8 == BM * BK && CPW * NT * 8 == BN * BK, "tile split");
   __shared__ __attribute__((aligned(16))) uint16_t xs[2][BM * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t ws[2][BN * LDK];
-  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, r = lane & 31, hh = lane >> 5;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int wm = (wv >> 1) * 64, wn = (wv & 1) * 64;
 
-  u32x4 xr[CPT], wr[CPT];
+  // output tile of this workgroup: XCD x = blockIdx % 8 takes tiles
+  // [x * per_xcd, (x + 1) * per_xcd), in groups of kGroupM tile rows
+  const int n_tm = (M + BM - 1) / BM, n_tn = (N + BN - 1) / BN;
+  const int per_xcd = (n_tm * n_tn + 7) / 8;
+  const int t = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+  if (t >= n_tm * n_tn) return;
+  const int grp = t / (kGroupM * n_tn), first_m = grp * kGroupM;
+  const int gsize = min(n_tm - first_m, kGroupM);
+  const int idx = t - grp * kGroupM * n_tn;
+  const int m0 = (first_m + idx % gsize) * BM, n0 = (idx / gsize) * BN;
+
+  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, r = lane & 31, hh = lane >> 5;
+  const int wm = (wv % WGM) * TM * 32, wn = (wv / WGM) * TN * 32;
+
+  // Loads read clamped (always valid) addresses, so the load sequence has no
+  // branches: rows past M or N only feed output rows and columns that are
+  // never stored, and chunks past K are zeroed when they are written to LDS.
+  u32x4 xr[CPX], wr[CPW];
   auto load = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * 256;
+    for (int i = 0; i < CPX; ++i) {
+      const int c = tid + i * NT;
       const int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
-      const bool kin = k0 + kc < K;
-      xr[i] = (m0 + row < M && kin) ? *(const u32x4*)(X + (int64_t)(m0 + row) * K + k0 + kc)
-                                    : u32x4{0, 0, 0, 0};
-      wr[i] = (n0 + row < N && kin) ? *(const u32x4*)(W + (int64_t)(n0 + row) * K + k0 + kc)
-                                    : u32x4{0, 0, 0, 0};
+      xr[i] = *(const u32x4*)(X + (int64_t)min(m0 + row, M - 1) * K + min(k0 + kc, K - 8));
+    }
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int c = tid + i * NT;
+      const int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
+      wr[i] = *(const u32x4*)(W + (int64_t)min(n0 + row, N - 1) * K + min(k0 + kc, K - 8));
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, int k0) {
+    const bool tail = k0 + BK > K;
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * 256;
-      const int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
-      *(u32x4*)&xs[buf][row * LDK + kc] = xr[i];
-      *(u32x4*)&ws[buf][row * LDK + kc] = wr[i];
+    for (int i = 0; i < CPX; ++i) {
+      const int c = tid + i * NT;
+      const int kc = (c % (BK / 8)) * 8;
+      const u32x4 v = tail && k0 + kc >= K ? u32x4{0, 0, 0, 0} : xr[i];
+      *(u32x4*)&xs[buf][(c / (BK / 8)) * LDK + kc] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int c = tid + i * NT;
+      const int kc = (c % (BK / 8)) * 8;
+      const u32x4 v = tail && k0 + kc >= K ? u32x4{0, 0, 0, 0} : wr[i];
+      *(u32x4*)&ws[buf][(c / (BK / 8)) * LDK + kc] = v;
     }
   };
 
-  f32x16 acc[2][2];   // [n sub-tile][m sub-tile], element (n, m)
+  f32x16 acc[TN][TM];   // [n sub-tile][m sub-tile], element (n, m)
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x16{};
 
   const int nk = (K + BK - 1) / BK;
   load(0);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    store(buf);                 // buffer last read two steps ago, one barrier before
-    __syncthreads();
+    store(buf, kt * BK);        // buffer last read two steps ago, one barrier before
     if (kt + 1 < nk) load((kt + 1) * BK);
+    __syncthreads();
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 wa[2], xb[2];
+      bf16x8 wa[TN], xb[TM];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TN; ++i)
         wa[i] = __builtin_bit_cast(
             bf16x8, *(const u32x4*)&ws[buf][(wn + 32 * i + r) * LDK + ks * 16 + 8 * hh]);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < TM; ++j)
         xb[j] = __builtin_bit_cast(
             bf16x8, *(const u32x4*)&xs[buf][(wm + 32 * j + r) * LDK + ks * 16 + 8 * hh]);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TN; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[i], xb[j], acc[i][j], 0, 0, 0);
     }
   }
   // acc[i][j] lane (r, hh), register q: n = wn + 32i + 8(q/4) + 4hh + q%4,
   // m = wm + 32j + r.
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < TM; ++j) {
     const int m = m0 + wm + 32 * j + r;
     if (m >= M) continue;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TN; ++i)
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         const int n = n0 + wn + 32 * i + 8 * q4 + 4 * hh;
         if (n >= N) continue;                      // N is a multiple of 8: whole group in or out
-        const int64_t idx = (int64_t)m * N + n;
+        const int64_t o = (int64_t)m * N + n;
         f32x4 v = {acc[i][j][4 * q4 + 0], acc[i][j][4 * q4 + 1], acc[i][j][4 * q4 + 2],
                    acc[i][j][4 * q4 + 3]};
         if (R) {
-          const u32x2 rb = *(const u32x2*)(R + idx);
+          const u32x2 rb = *(const u32x2*)(R + o);
           v[0] += bf16_to_f32((uint16_t)(rb[0] & 0xFFFF));
           v[1] += bf16_to_f32((uint16_t)(rb[0] >> 16));
           v[2] += bf16_to_f32((uint16_t)(rb[1] & 0xFFFF));
           v[3] += bf16_to_f32((uint16_t)(rb[1] >> 16));
         }
-        *(bf16x4*)(Y + idx) = __builtin_convertvector(v, bf16x4);
+        *(bf16x4*)(Y + o) = __builtin_convertvector(v, bf16x4);
       }
   }
+}
+
+template <int WGM, int WGN, int TM, int TN, int MINB>
+void launch_tiles(int m, int n, int k, const void* x, const void* w, const void* r, void* y,
+                  hipStream_t s) {
+  constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
+  const int tiles = ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_bf16_kernel<WGM, WGN, TM, TN, MINB>), dim3(8 * ((tiles + 7) / 8)),
+                     dim3(WGM * WGN * 64), 0, s, m, n, k, (const uint16_t*)x, (const uint16_t*)w,
+                     (const uint16_t*)r, (uint16_t*)y);
 }
 
 }  // namespace
 
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s) {
-  dim3 grid((n + BN - 1) / BN, (m + BM - 1) / BM);
-  hipLaunchKernelGGL(gemm_bf16_kernel, grid, dim3(256), 0, s, m, n, k, (const uint16_t*)x,
-                     (const uint16_t*)w, (const uint16_t*)r, (uint16_t*)y);
+  // 256 x 256 tiles when they give every CU at least one (256 CUs), else 128 x 128
+  const int64_t big = (int64_t)((m + 255) / 256) * ((n + 255) / 256);
+  if (big >= 256)
+    launch_tiles<4, 2, 2, 4, 1>(m, n, k, x, w, r, y, s);
+  else
+    launch_tiles<2, 2, 2, 2, 2>(m, n, k, x, w, r, y, s);
   return hipGetLastError();
 }
 

@@ -24,7 +24,7 @@ def _f64(t: torch.Tensor) -> np.ndarray:
 
 @pytest.mark.parametrize("m,n,k,res", [(1, 8, 8, False), (37, 136, 72, True), (128, 128, 64, False),
                                        (300, 1024, 520, True), (257, 264, 1024, False),
-                                       (1000, 1024, 8192, True)])
+                                       (1000, 1024, 8192, True), (4100, 4104, 200, True)])
 def test_gemm_matches_fp64(m, n, k, res):
     from paper_2609_04875_amd import gemm_bf16
     rng = np.random.default_rng(m * 7 + n)
@@ -57,6 +57,18 @@ def test_gemm_rows_are_independent_and_deterministic():
     assert torch.equal(full, gemm_bf16(x, w))
     part = gemm_bf16(x[101:230].contiguous(), w)
     assert torch.equal(part, full[101:230])
+
+
+def test_gemm_tile_shapes_agree_bitwise():
+    """A product large enough for the 256 x 256 tiles (16 x 16 of them) and a
+    slice of its rows, which runs the 128 x 128 tiles: same bits per row."""
+    from paper_2609_04875_amd import gemm_bf16
+    rng = np.random.default_rng(5)
+    x = _bf16_dev(rng.standard_normal((4096, 1024)))
+    w = _bf16_dev(rng.standard_normal((4096, 1024)) / 32)
+    full = gemm_bf16(x, w)
+    part = gemm_bf16(x[1000:1300].contiguous(), w)
+    assert torch.equal(part, full[1000:1300])
 
 
 def test_gemm_residual_may_alias_output():
