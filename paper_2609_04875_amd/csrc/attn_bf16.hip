@@ -139,7 +139,8 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
 #pragma unroll
     for (int ds = 0; ds < D / 16; ++ds) {
       u32x4 raw = valid ? *(const u32x4*)(qg + 16 * ds) : u32x4{0, 0, 0, 0};
-      qb[ds] = __builtin_bit_cast(bf16x8, raw);
+      const f32x8 qx = __builtin_convertvector(__builtin_bit_cast(bf16x8, raw), f32x8) * a.scale_log2;
+      qb[ds] = __builtin_convertvector(qx, bf16x8);   // Q scaled by the softmax scale * log2(e), rounded once
     }
   }
 
@@ -210,13 +211,16 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
-  float m = -INFINITY, l = 0.f;
-  const float c2 = a.scale_log2;
+  // S^T accumulators start at -m_use (cinit), so they hold s * c - m_use and
+  // the exponentials need no subtraction; m_use moves only with the lazy
+  // rescale, when the tile just computed is shifted by the same amount.
+  float m = -INFINITY, l = 0.f, m_use = 0.f;
+  f32x16 cinit = {};
 
   // S^T = K Q^T for one 64-key tile: two independent 32-key accumulators.
   auto qk = [&](int buf, f32x16 (&s)[2]) {
-    s[0] = f32x16{};
-    s[1] = f32x16{};
+    s[0] = cinit;
+    s[1] = cinit;
     const int kr = (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);   // pi(r): bits 2 and 3 swapped
     const uint16_t* kp = &k_lds[buf][kr * KLD + 8 * hh];
     constexpr int N = D / 16;
@@ -306,12 +310,20 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
     for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kh][i]);
-    mx = fmaxf(mx, xor32(mx)) * c2;                // tile max of the row, log2 units
+    mx = fmaxf(mx, xor32(mx)) + m_use;             // tile max of the row, log2 units
     const bool bump = mx > m + kSlack;             // first tile: m = -inf
     const float m_new = bump ? mx : m;
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float mu = m_new == -INFINITY ? 0.f : m_new;
+    const float delta = mu - m_use;                // 0 unless this row moved its max
+    m_use = mu;
     const float alpha = bump ? __builtin_amdgcn_exp2f(m - m_use) : 1.f;
     m = m_new;
+    if (__ballot(bump)) {
+      s[0] -= delta;
+      s[1] -= delta;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) cinit[i] = -m_use;
+    }
     // P = exp2(s*c - m) rounded to bf16; the row sum adds exactly those values.
     bf16x8 pb[KT / 16];
     float ps0 = 0.f, ps1 = 0.f;
@@ -320,7 +332,7 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
       const int kh = ks >> 1, o8 = (ks & 1) * 8;
       f32x8 pv8;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) pv8[j] = __builtin_amdgcn_exp2f(fmaf(s[kh][o8 + j], c2, -m_use));
+      for (int j = 0; j < 8; ++j) pv8[j] = __builtin_amdgcn_exp2f(s[kh][o8 + j]);
       pb[ks] = __builtin_convertvector(pv8, bf16x8);
       const bf16x2* p2 = (const bf16x2*)&pb[ks];
       ps0 = __builtin_amdgcn_fdot2_f32_bf16(p2[0], kOnes, ps0, false);

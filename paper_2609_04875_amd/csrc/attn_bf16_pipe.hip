@@ -17,8 +17,12 @@
 //   registers); a lane holds one query column and 16 keys of each 32-key half,
 //   so row max and row sum are in-lane plus one exchange between lane halves.
 //   Online softmax in base 2 with a lazy rescale (the running max moves only
-//   when a tile exceeds it by more than 2^8); P is rounded to bf16 and the row
-//   sum adds exactly those values; O^T += V^T P^T.  Accumulator row i of S^T
+//   when a tile exceeds it by more than 2^8).  Q is scaled by the softmax
+//   scale * log2(e) once, when it is loaded, and every S accumulator starts
+//   at -m (m: the row's current reference max), so S holds s * c - m and the
+//   exponentials take it directly; when m moves, the tile that moved it is
+//   shifted by the same amount.  P is rounded to bf16 and the row sum adds
+//   exactly those values; O^T += V^T P^T.  Accumulator row i of S^T
 //   is key pi(i) (bits 2 and 3 of i swapped), so a lane's P^T registers hold
 //   8 consecutive keys of each 16-key group and V^T sits in LDS in natural
 //   key order: every operand is one 16-byte read.
@@ -124,7 +128,8 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
 #pragma unroll
     for (int ds = 0; ds < NDS; ++ds) {
       u32x4 raw = valid[b] ? *(const u32x4*)(qg + 16 * ds) : u32x4{0, 0, 0, 0};
-      qf[b][ds] = __builtin_bit_cast(bf16x8, raw);
+      f32x8 qx = __builtin_convertvector(__builtin_bit_cast(bf16x8, raw), f32x8) * a.scale_log2;
+      qf[b][ds] = __builtin_convertvector(qx, bf16x8);   // Q scaled by scale * log2(e), rounded once
     }
   }
 
@@ -196,19 +201,20 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   };
   auto commit_next = [&](int x) { store_tile((x + 2) % kPBuf, (x + 2) * KT); };
 
-  const float c2 = a.scale_log2;
   f32x16 oacc[QB][NDB];
 #pragma unroll
   for (int b = 0; b < QB; ++b)
 #pragma unroll
     for (int db = 0; db < NDB; ++db) oacc[b][db] = f32x16{};
   float m[QB], l[QB], alpha[QB], m_use[QB];
+  f32x16 cinit[QB];     // -m_use in every element: the start value of each S accumulator
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
     m[b] = -INFINITY;
     l[b] = 0.f;
     alpha[b] = 1.f;
     m_use[b] = 0.f;
+    cinit[b] = f32x16{};
   }
 
   const int kr = (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);   // pi(r): bits 2 and 3 swapped
@@ -230,38 +236,46 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int i = 0; i < 16; ++i) x = fmaxf(x, s[b][kh][i]);
-      mx[b] = fmaxf(x, xor32(x)) * c2;
+      mx[b] = fmaxf(x, xor32(x)) + m_use[b];   // S holds s * c - m_use
     }
   };
-  auto apply_max = [&](const float (&mx)[QB]) {
+  auto apply_max = [&](const float (&mx)[QB], f32x16 (&st)[QB][2]) {
     bool any = false;
+    float delta[QB];
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
       const bool bump = mx[b] > m[b] + kPSlack;
       const float m_new = bump ? mx[b] : m[b];
-      m_use[b] = m_new == -INFINITY ? 0.f : m_new;
+      const float mu = m_new == -INFINITY ? 0.f : m_new;
+      delta[b] = mu - m_use[b];
+      m_use[b] = mu;
       alpha[b] = bump ? __builtin_amdgcn_exp2f(m[b] - m_use[b]) : 1.f;
       m[b] = m_new;
       any = any || bump;
     }
     if (__ballot(any)) {
 #pragma unroll
-      for (int b = 0; b < QB; ++b)
+      for (int b = 0; b < QB; ++b) {
 #pragma unroll
         for (int db = 0; db < NDB; ++db) oacc[b][db] *= alpha[b];
+        st[b][0] -= delta[b];
+        st[b][1] -= delta[b];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) cinit[b][i] = -m_use[b];
+      }
     }
   };
-  auto update_max = [&](const f32x16 (&s)[QB][2]) {
+  auto update_max = [&](f32x16 (&s)[QB][2]) {
     float mx[QB];
     row_max(s, mx);
-    apply_max(mx);
+    apply_max(mx, s);
   };
   // P for 16 keys (registers o8 .. o8+7 of one 32-key half), rounded to bf16,
   // with the row-sum terms added in the fixed order.
   auto expo = [&](const f32x16& s, int o8, int b, float& ps0, float& ps1) {
     f32x8 pv8;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) pv8[j] = __builtin_amdgcn_exp2f(fmaf(s[o8 + j], c2, -m_use[b]));
+    for (int j = 0; j < 8; ++j) pv8[j] = __builtin_amdgcn_exp2f(s[o8 + j]);
     const bf16x8 p = __builtin_convertvector(pv8, bf16x8);
     const bf16x2* p2 = (const bf16x2*)&p;
     ps0 = __builtin_amdgcn_fdot2_f32_bf16(p2[0], kOnes, ps0, false);
@@ -290,7 +304,7 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   f32x16 sa[QB][2], sb[QB][2];
   auto qk = [&](int buf, f32x16 (&s)[QB][2]) {
 #pragma unroll
-    for (int b = 0; b < QB; ++b) s[b][0] = s[b][1] = f32x16{};
+    for (int b = 0; b < QB; ++b) s[b][0] = s[b][1] = cinit[b];
 #pragma unroll
     for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
@@ -318,7 +332,7 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
     for (int b = 0; b < QB; ++b) {
       ps0[b] = 0.f;
       ps1[b] = 0.f;
-      sn[b][0] = sn[b][1] = f32x16{};
+      sn[b][0] = sn[b][1] = cinit[b];
     }
     // phase A: 32 products of S(t+1), 16 K operand reads; exponentials of
     // keys 0..31 of S(t) (both blocks)
@@ -360,7 +374,7 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       asm volatile("" ::"v"(l[b]));
     }
     commit_next(t);
-    apply_max(mx);
+    apply_max(mx, sn);
   };
   // Finish a tile whose S is computed and whose max is taken.
   auto finish = [&](int t, const f32x16 (&sc)[QB][2]) {
