@@ -211,16 +211,15 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
-  // S^T accumulators start at -m_use (cinit), so they hold s * c - m_use and
-  // the exponentials need no subtraction; m_use moves only with the lazy
+  // S^T accumulators start at -m_use, so they hold s * c - m_use and the
+  // exponentials need no subtraction; m_use moves only with the lazy
   // rescale, when the tile just computed is shifted by the same amount.
   float m = -INFINITY, l = 0.f, m_use = 0.f;
-  f32x16 cinit = {};
 
   // S^T = K Q^T for one 64-key tile: two independent 32-key accumulators.
   auto qk = [&](int buf, f32x16 (&s)[2]) {
-    s[0] = cinit;
-    s[1] = cinit;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[0][i] = s[1][i] = -m_use;
     const int kr = (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);   // pi(r): bits 2 and 3 swapped
     const uint16_t* kp = &k_lds[buf][kr * KLD + 8 * hh];
     constexpr int N = D / 16;
@@ -321,8 +320,6 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
     if (__ballot(bump)) {
       s[0] -= delta;
       s[1] -= delta;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) cinit[i] = -m_use;
     }
     // P = exp2(s*c - m) rounded to bf16; the row sum adds exactly those values.
     bf16x8 pb[KT / 16];
