@@ -27,9 +27,9 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
-# Per-source options.  The pipelined prefill kernel runs one wave per SIMD and
-# reads every product's result with VALU instructions (softmax, rescale), so
-# its matrix results must live in VGPRs: left to its heuristics the compiler
+# Per-source options.  The pipelined prefill kernel reads every product's
+# result with VALU instructions (softmax, rescale), so its matrix results must
+# live in VGPRs: left to its heuristics the compiler
 # places them in AGPRs and copies them back on every step.
 EXTRA = {"attn_bf16_pipe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
