@@ -407,7 +407,8 @@ def replay_gain(T: int, tau: int) -> float:
 # stacked random-init layers (reading: the paper defines no layer)            #
 # --------------------------------------------------------------------------- #
 def stacked_layers(x: np.ndarray, layers, n_q_heads: int, n_kv_heads: int, head_dim: int,
-                   scale: float, pos0: int = 0, cache: Optional[List[Tuple[np.ndarray, np.ndarray]]] = None):
+                   scale: float, pos0: int = 0, cache: Optional[List[Tuple[np.ndarray, np.ndarray]]] = None,
+                   record: Optional[list] = None):
     """F for the stacked workload: per layer, with bf16 storage points mirrored,
 
         Q = bf16(x Wq), K = bf16(x Wk), V = bf16(x Wv)
@@ -418,7 +419,8 @@ def stacked_layers(x: np.ndarray, layers, n_q_heads: int, n_kv_heads: int, head_
     holding bf16 values); ``layers`` is a list of (Wq, Wk, Wv, Wo) fp64 arrays;
     ``cache`` gives each layer's K/V for positions 0 .. pos0-1 (the cropped
     prefix), or None when pos0 == 0.  Returns (x_out, per-layer (K, V) of the
-    n new tokens).  Matrix products are library matmuls in fp64.
+    n new tokens).  Matrix products are library matmuls in fp64.  ``record``
+    (a list), when given, receives each layer's O [n, Hq * d].
     """
     n = x.shape[0]
     new_kv = []
@@ -432,6 +434,8 @@ def stacked_layers(x: np.ndarray, layers, n_q_heads: int, n_kv_heads: int, head_
         else:
             kk, vv = k, v
         o = bf16_round(attention(q, kk, vv, pos0, scale)).reshape(n, n_q_heads * head_dim)
+        if record is not None:
+            record.append(o)
         x = bf16_round(x + o @ wo)
         new_kv.append((k, v))
     return x, new_kv

@@ -384,13 +384,14 @@ constexpr int kGroup = 8;
 template <int D, typename TO>
 __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, TO* __restrict__ og) {
   constexpr int TPR = D / 8;                       // threads per row
-  const int64_t row = (int64_t)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+  const int64_t row = a.row_begin + (int64_t)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
   const int c0 = (threadIdx.x % TPR) * 8;
-  if (row >= a.n_rows) return;
+  if (row >= a.row_end) return;
   const int tok = (int)(row / a.n_q_heads);        // packed query token
-  int ei = 0;                                      // entries are not sorted by q_off
+  int ei = -1;                                     // entries are not sorted by q_off
   for (int i = 0; i < a.n; ++i)
     if (tok >= a.e[i].q_off && tok < a.e[i].q_off + a.e[i].q_len) ei = i;
+  if (ei < 0) return;                              // a row of no entry of this launch
   const AttnEntry e = a.e[ei];
   const int qpos = e.prefix + (tok - e.q_off);
   const int ns = min(a.n_splits, qpos / a.split_len + 1);
@@ -468,9 +469,10 @@ static hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s) {
-  if (a.n_rows <= 0) return hipSuccess;
+  if (a.row_begin < 0 || a.row_end > a.n_rows) return hipErrorInvalidValue;
+  if (a.row_end <= a.row_begin) return hipSuccess;
   const int rows_per_block = 256 / (a.head_dim / 8);
-  dim3 grid((a.n_rows + rows_per_block - 1) / rows_per_block);
+  dim3 grid((a.row_end - a.row_begin + rows_per_block - 1) / rows_per_block);
   if (a.head_dim == 128 && f32_out)
     hipLaunchKernelGGL((split_combine_kernel<128, float>), grid, dim3(256), 0, s, a, (float*)a.o);
   else if (a.head_dim == 64 && f32_out)

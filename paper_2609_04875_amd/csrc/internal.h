@@ -132,6 +132,10 @@ struct AttnArgs {
   int32_t n_splits;
   int32_t split_len;
   int32_t n_rows;
+  // Packed query rows [row_begin, row_end) belong to this launch's entries
+  // (a call with more than kMaxSeqsPerLaunch sequences is several launches,
+  // each owning one contiguous run of rows); the combine touches only those.
+  int32_t row_begin, row_end;
   float* ws_acc;
   float* ws_ml;
   AttnEntry e[kMaxSeqsPerLaunch];

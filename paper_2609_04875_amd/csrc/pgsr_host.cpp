@@ -105,17 +105,13 @@ void mirror_crop(pgsr_pool* p, int32_t s, int32_t L) {
 
 // Blocks a crop of these sequences would push (the mirror is left unchanged).
 int64_t count_freed(const pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_lens) {
-  std::vector<std::pair<int32_t, int32_t>> dec;   // (block, decrements so far)
+  std::unordered_map<int32_t, int32_t> dec;   // block -> decrements so far
   int64_t freed = 0;
   for (int32_t i = 0; i < n; ++i) {
     const int32_t s = seqs[i], keep = cdiv(new_lens[i], p->B);
     for (int32_t j = keep; j < p->h_nalloc[s]; ++j) {
       const int32_t b = p->h_tab[(size_t)s * p->max_bps + j];
-      int32_t k = 0;
-      for (auto& d : dec)
-        if (d.first == b) k = ++d.second;
-      if (k == 0) dec.push_back({b, k = 1});
-      if (p->h_ref[b] - k == 0) ++freed;
+      if (p->h_ref[b] - ++dec[b] == 0) ++freed;
     }
   }
   return freed;
@@ -377,6 +373,10 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.n_splits = 1;
     a.split_len = 0;
     a.n_rows = off * p->hq;                        // packed query rows of the whole call
+    // this launch's sequences are consecutive in call order, so their rows
+    // form one contiguous run of the packed queries
+    a.row_begin = segs[base].q_off * p->hq;
+    a.row_end = (segs[base + cnt - 1].q_off + segs[base + cnt - 1].q_len) * p->hq;
     if (decode) {
       int32_t max_key = 0;
       for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);

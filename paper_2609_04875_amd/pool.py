@@ -30,12 +30,30 @@ def _stream_ptr(stream: Optional[torch.cuda.Stream], device: Optional[int] = Non
     return torch._C._cuda_getCurrentRawStream(idx) or None
 
 
-def _dev_ptr(t: Optional[torch.Tensor], dtype, name: str) -> Optional[int]:
+def _dev_ptr(t: Optional[torch.Tensor], dtype, name: str, device: Optional[int] = None,
+             numel: Optional[int] = None) -> Optional[int]:
+    """Device address of ``t`` after checking what the C ABI cannot: dtype,
+    contiguity, that it is on ``device`` (when given) and holds exactly
+    ``numel`` elements (when given).  The library takes raw pointers, so a
+    short tensor would otherwise be read or written past its end."""
     if t is None:
+        if numel:
+            raise ValueError(f"{name} is None but {numel} elements are needed")
         return None
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} holds {t.numel()} elements; the call needs exactly {numel}")
     if not t.is_cuda or not t.is_contiguous() or t.dtype != dtype:
         raise ValueError(f"{name} must be a contiguous {dtype} CUDA tensor")
+    if device is not None and t.device.index != device:
+        raise ValueError(f"{name} is on cuda:{t.device.index}; the pool is on cuda:{device}")
     return t.data_ptr() if t.numel() else None
+
+
+def prefill_sizes(n_q_heads: int, n_kv_heads: int, head_dim: int, q_lens: Sequence[int]):
+    """Elements that q / o and k / v of a prefill call must hold:
+    sum(q_lens) tokens of [n_q_heads][head_dim] and [n_kv_heads][head_dim]."""
+    tot = sum(int(x) for x in q_lens)
+    return tot * n_q_heads * head_dim, tot * n_kv_heads * head_dim
 
 
 class KVPool:
@@ -133,11 +151,17 @@ class KVPool:
                                   _stream_ptr(stream, self._dev))
 
     def _prefill(self, fn, layer, seqs, q_lens, q, k, v, o, scale, commit, stream) -> int:
-        dt = self.dtype
+        dt, dv = self.dtype, self._dev
+        if len(q_lens) != len(seqs):
+            raise ValueError(f"{len(seqs)} sequences but {len(q_lens)} lengths")
+        if any(int(x) < 0 for x in q_lens):
+            raise ValueError("negative query length")
+        nq, nkv = prefill_sizes(self.hq, self.hkv, self.d, q_lens)
         return fn(self._h, layer, len(seqs), N.int32_array(seqs), N.int32_array(q_lens),
-                  _dev_ptr(q, dt, "q"), _dev_ptr(k, dt, "k"), _dev_ptr(v, dt, "v"),
-                  _dev_ptr(o, dt, "o"), float(scale), N.COMMIT if commit else 0,
-                  ctypes.byref(self.recomputed_tokens), _stream_ptr(stream, self._dev))
+                  _dev_ptr(q, dt, "q", dv, nq), _dev_ptr(k, dt, "k", dv, nkv),
+                  _dev_ptr(v, dt, "v", dv, nkv), _dev_ptr(o, dt, "o", dv, nq), float(scale),
+                  N.COMMIT if commit else 0, ctypes.byref(self.recomputed_tokens),
+                  _stream_ptr(stream, dv))
 
     def replay(self, layer: int, seqs, q_lens, q, k, v, o, scale: float, commit: bool = True,
                stream=None) -> int:
@@ -181,10 +205,11 @@ def gemm_bf16(x: torch.Tensor, w: torch.Tensor, r: Optional[torch.Tensor] = None
     n, k2 = w.shape
     if k2 != k:
         raise ValueError("inner dimensions differ")
+    dv = x.device.index
     if out is None:
         out = torch.empty((m, n), dtype=torch.bfloat16, device=x.device)
-    N.check(N.lib.pgsr_gemm_bf16(m, n, k, _dev_ptr(x, torch.bfloat16, "x"),
-                                 _dev_ptr(w, torch.bfloat16, "w"),
-                                 _dev_ptr(r, torch.bfloat16, "r") if r is not None else None,
-                                 _dev_ptr(out, torch.bfloat16, "out"), _stream_ptr(stream)))
+    bf = torch.bfloat16
+    N.check(N.lib.pgsr_gemm_bf16(m, n, k, _dev_ptr(x, bf, "x"), _dev_ptr(w, bf, "w", dv),
+                                 _dev_ptr(r, bf, "r", dv, m * n) if r is not None else None,
+                                 _dev_ptr(out, bf, "out", dv, m * n), _stream_ptr(stream, dv)))
     return out

@@ -38,8 +38,10 @@ class StackedReplay:
             self._buf[name] = t
         return t.view(-1)[: int(torch.tensor(shape).prod())].view(shape)
 
-    def _run(self, fn, seq: int, x: torch.Tensor, scale: float) -> torch.Tensor:
-        """Push the token states x [n, dm] through every layer; returns the new x."""
+    def _run(self, fn, seq: int, x: torch.Tensor, scale: float,
+             record: Optional[list] = None) -> torch.Tensor:
+        """Push the token states x [n, dm] through every layer; returns the new x.
+        ``record`` (a list) receives a copy of each layer's attention output."""
         n = x.shape[0]
         q = self._scratch("q", (n, self.hq * self.d))
         k = self._scratch("k", (n, self.hkv * self.d))
@@ -54,16 +56,18 @@ class StackedReplay:
             rc = fn(li, [seq], [n], q, k, v, o, scale, commit=(li == last))
             if rc:
                 raise N.PgsrError(rc, N.lib.pgsr_last_error().decode())
+            if record is not None:
+                record.append(o.clone())
             gemm_bf16(o, wo, r=x, out=x)               # x <- x + O Wo
         return x
 
-    def replay(self, seq: int, x: torch.Tensor, scale: float) -> torch.Tensor:
+    def replay(self, seq: int, x: torch.Tensor, scale: float, record: Optional[list] = None) -> torch.Tensor:
         """Replay tokens at positions len(seq) .. len(seq)+n-1 (Algorithm 1, replay loop)."""
-        return self._run(self.pool.replay, seq, x, scale)
+        return self._run(self.pool.replay, seq, x, scale, record)
 
-    def full_reset(self, seq: int, x: torch.Tensor, scale: float) -> torch.Tensor:
+    def full_reset(self, seq: int, x: torch.Tensor, scale: float, record: Optional[list] = None) -> torch.Tensor:
         """Baseline B5: crop to 0 (on the first layer) and replay all of x."""
-        return self._run(self.pool.full_reset, seq, x, scale)
+        return self._run(self.pool.full_reset, seq, x, scale, record)
 
     def crop(self, seqs: List[int], new_lens: List[int]) -> int:
         return self.pool.crop(seqs, new_lens)

@@ -83,3 +83,36 @@ def test_null_pool_and_gemm_validation(native):
 
 def test_prefill_kernel_choice_is_validated(native):
     assert native.lib.pgsr_pool_set_prefill_kernel(None, 0) == native.EINVAL
+
+
+def test_binding_rejects_tensors_of_the_wrong_size_or_device():
+    """The C ABI takes raw pointers, so the binding checks what it cannot:
+    exact element counts for the call's token total, and the pool's device."""
+    import torch
+    from paper_2609_04875_amd.pool import _dev_ptr, prefill_sizes
+
+    assert prefill_sizes(32, 8, 128, [3, 0, 5]) == (8 * 32 * 128, 8 * 8 * 128)
+    q = torch.zeros((7, 32, 128), dtype=torch.bfloat16)      # one token short of 3 + 0 + 5
+    nq, nkv = prefill_sizes(32, 8, 128, [3, 0, 5])
+    with pytest.raises(ValueError, match="exactly"):
+        _dev_ptr(q, torch.bfloat16, "q", None, nq)
+    with pytest.raises(ValueError, match="exactly"):
+        _dev_ptr(torch.zeros((9, 8, 128), dtype=torch.bfloat16), torch.bfloat16, "k", None, nkv)
+    with pytest.raises(ValueError, match="needed"):
+        _dev_ptr(None, torch.bfloat16, "o", None, nq)
+    with pytest.raises(ValueError, match="CUDA"):              # right size, but host memory
+        _dev_ptr(torch.zeros((8, 32, 128), dtype=torch.bfloat16), torch.bfloat16, "q", None, nq)
+
+    class OnOtherDevice:                                      # stands in for a tensor on cuda:1
+        is_cuda = True
+        dtype = torch.bfloat16
+        device = torch.device("cuda", 1)
+
+        def numel(self):
+            return nq
+
+        def is_contiguous(self):
+            return True
+
+    with pytest.raises(ValueError, match="cuda:1"):
+        _dev_ptr(OnOtherDevice(), torch.bfloat16, "q", 0, nq)

@@ -163,6 +163,34 @@ def test_negative_control_without_crop_differs():
     assert mx > 0.2 and rel > 0.1, (mx, rel)
 
 
+def test_negative_control_span_only_excision_differs():
+    """The span-only invalidation boundary of the ablation (Section 4, Table 4):
+    cut the target's own slots out of the contaminated cache but keep the KV of
+    everything computed after it.  On the GPU the kept state is the prefix
+    followed by the contaminated suffix past the target span; its outputs must
+    differ from the full reset of the sanitized trajectory by far more than the
+    tolerance (the comparison has power), while matching the oracle for that
+    same (wrong) state."""
+    geom = W.AttnGeometry(32, 8, 128)
+    rng = np.random.default_rng(25)
+    P, S, Tc, z = 500, 120, 700, 3                 # the target: the first 3 contaminated tokens
+    ep = W.draw_episode(rng, geom, "bf16", P, S, Tc)
+    scale = 128 ** -0.5
+    pool = make_pool(geom, "bf16", 2 * _blocks(Tc) + 8, 2, 128)
+    span = {x: np.concatenate([getattr(ep, x)[:P], getattr(ep, "c" + x)[z:]]) for x in ("q", "k", "v")}
+    sq, sk, sv = (dev(span[x], "bf16") for x in ("q", "k", "v"))
+    so = torch.empty_like(sq)
+    assert pool.replay(0, [0], [Tc - z], sq, sk, sv, so, scale) == 0
+    full = _full_reset(pool, ep, 1, scale)
+    n = min(S, Tc - P - z)
+    mx, rel = errors(so[P:P + n].float().cpu().numpy(), full[P:P + n].float().cpu().numpy().astype(np.float64))
+    log(f"span-only excision vs full reset: max|d| {mx:.3f}, rel {rel:.3f}")
+    assert mx > 0.2 and rel > 0.1, (mx, rel)
+    ref = oracle.attention(*(storage_f64(span[x][P:] if x == "q" else span[x], "bf16") for x in ("q", "k", "v")),
+                           P, scale)
+    assert_close(so[P:].float().cpu().numpy(), ref, "bf16", "span-only state")
+
+
 def test_varlen_ragged_batch_reduced_lengths():
     w = W.workload("ragged16_llama8b_bf16")
     eps = W.ragged_episodes(w, scale_len=1 / 16)
@@ -196,10 +224,12 @@ def _sample_rows(rng, S, hq, n):
     return np.unique(rows)
 
 
-def test_llama8b_workload_full_size_sampled():
+def test_llama8b_workload_full_size_every_row():
     """8B geometry at its real shape: crop at 8189 (13 valid slots in the tail
-    block), replay 2048; sampled rows against the oracle, every row against
-    the GPU full reset of 10237 tokens (bitwise)."""
+    block), replay 2048; every one of the 2048 x 32 output rows against the
+    oracle, with the bf16 acceptance metric (max |d| and sum|d| / sum|ref|)
+    taken over the whole output, and every row against the GPU full reset of
+    10237 tokens (bitwise)."""
     w = W.workload("llama8b_p8189_s2048_bf16")
     log(f"workload {w.name}")
     ep = W.single_episode(w)
@@ -208,13 +238,69 @@ def test_llama8b_workload_full_size_sampled():
     assert pool.seq_len(0) == 8189
     o = _replay(pool, ep, 0, w.scale)
     assert pool.seq_len(0) == 10237
-    rng = np.random.default_rng(5)
-    rows = _sample_rows(rng, ep.suffix, 32, 96)
-    ref = oracle_suffix(ep, w.scale, rows=rows)
-    got = o.float().cpu().numpy().reshape(-1, 128)[rows]
+    got = o.float().cpu().numpy()
+    log(f"{w.name}: oracle on all {ep.suffix} x 32 rows")
+    ref = oracle_suffix(ep, w.scale)
+    mx, rel = errors(got, ref)
+    log(f"{w.name}: whole output max|d| {mx:.3e}, sum|d|/sum|ref| {rel:.3e}")
     assert_close(got, ref, "bf16", w.name)
     full = _full_reset(pool, ep, 1, w.scale)
     assert torch.equal(full[ep.prefix:], o)
+
+
+def _ragged_tokens(rng, P, S, tile=64):
+    """Suffix tokens to check in one episode: the first and last, the tokens
+    on both sides of every query-tile edge near the ends, those whose absolute
+    position straddles a 64-key tile edge (first and last such), and 32 at
+    random."""
+    t = [0, 1, tile - 1, tile, S - tile - 1, S - tile, S - 2, S - 1]
+    first_edge = (-P) % tile                       # (P + t) % 64 == 0
+    t += [first_edge - 1, first_edge, first_edge + tile - 1]
+    last_edge = first_edge + ((S - 1 - first_edge) // tile) * tile
+    t += [last_edge - 1, last_edge]
+    t += rng.integers(0, S, size=32).tolist()
+    return np.unique(np.clip(np.asarray(t), 0, S - 1))
+
+
+def test_ragged_workload_full_size_sampled():
+    """The 16-episode ragged batch at its configured lengths (T in [4096, 16384],
+    about 82k suffix tokens) in one varlen launch; in every episode the first,
+    last, tile-edge and diagonal-straddling tokens plus 32 random ones, all 32
+    heads, against the oracle."""
+    w = W.workload("ragged16_llama8b_bf16")
+    log(f"workload {w.name}: drawing 16 episodes")
+    eps = W.ragged_episodes(w)
+    n = len(eps)
+    log("ragged: " + ", ".join(f"({e.prefix},{e.suffix})" for e in eps))
+    tot_blocks = sum(_blocks(e.t_contaminated) + _blocks(e.t_sanitized) for e in eps)
+    pool = make_pool(w.geometry, "bf16", tot_blocks + 8, n, 1100)
+    for i, ep in enumerate(eps):
+        contaminated_then_crop(pool, ep, i, w.scale)
+    order = list(range(n))[::-1]
+    q = torch.cat([dev(eps[i].q[eps[i].prefix:], "bf16") for i in order])
+    k = torch.cat([dev(eps[i].k[eps[i].prefix:], "bf16") for i in order])
+    v = torch.cat([dev(eps[i].v[eps[i].prefix:], "bf16") for i in order])
+    o = torch.empty_like(q)
+    before = pool.recomputed_tokens.value
+    assert pool.replay(0, order, [eps[i].suffix for i in order], q, k, v, o, w.scale) == 0
+    assert pool.recomputed_tokens.value - before == sum(e.suffix for e in eps)
+    got = o.float().cpu().numpy().reshape(-1, 32, 128)
+    del q, k, v, o
+    rng = np.random.default_rng(8)
+    off = 0
+    all_got, all_ref = [], []
+    for i in order:
+        ep = eps[i]
+        toks = _ragged_tokens(rng, ep.prefix, ep.suffix)
+        rows = (toks[:, None] * 32 + np.arange(32)[None, :]).reshape(-1)
+        ref = oracle_suffix(ep, w.scale, rows=rows)
+        g = got[off:off + ep.suffix].reshape(-1, 128)[rows]
+        assert_close(g, ref, "bf16", f"episode {i} (P={ep.prefix}, S={ep.suffix})")
+        all_got.append(g)
+        all_ref.append(ref)
+        off += ep.suffix
+    mx, rel = errors(np.concatenate(all_got), np.concatenate(all_ref))
+    log(f"{w.name}: {sum(x.shape[0] for x in all_got)} rows, max|d| {mx:.3e}, rel {rel:.3e}")
 
 
 def test_long_horizon_chunked_full_size_sampled():

@@ -120,3 +120,56 @@ def test_stack_replay_matches_oracle_and_full_reset():
     d = np.abs(got - want)
     assert d.max() <= 2.0 ** -6 * np.abs(want).max(), (d.max(), np.abs(want).max())
     assert d.sum() / np.abs(want).sum() <= 1e-2
+
+
+def test_stack_at_the_70b_geometry_matches_oracle():
+    """The stacked workload's own geometry (64 query / 8 KV heads, d 128,
+    d_model 8192) at a reduced T = 2048 and 2 layers: crop to 25 % and 95 % of
+    T (the latter unaligned) and replay, against the oracle's stack over the
+    whole sanitized trajectory; each layer's attention output also within the
+    bf16 attention tolerance (max |d| <= 2e-2, sum|d| / sum|ref| <= 1e-2), and
+    the replays bitwise equal to the GPU full reset (Theorem 1)."""
+    from paper_2609_04875_amd import StackedReplay
+    base = W.workload("stack70b_8layer_t16384_bf16")
+    T, L = 2048, 2
+    geom, dm = base.geometry, base.d_model
+    w = W.Workload("stack70b_2layer_t2048", geom, "bf16", seed=base.seed, n_layers=L, d_model=dm, t_total=T)
+    log(f"70B-geometry stack: T={T}, {L} layers, d_model {dm}")
+    x0, xc, ws = W.stack_inputs(w)
+    f32 = lambda b: W.bf16_bits_to_f32(b)
+    dev = lambda b: torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).view(torch.bfloat16).cuda()
+    wdev = [tuple(dev(np.ascontiguousarray(m.T)) for m in layer) for layer in ws]   # [out][in]
+    nb = -(-T // 16)
+    stack = StackedReplay(wdev, geom.n_q_heads, geom.n_kv_heads, geom.head_dim,
+                          n_blocks=3 * nb + 8, max_seqs=3, max_blocks_per_seq=nb + 2)
+    scale = base.scale
+    xs = dev(x0)
+    full_att = []
+    full = stack.full_reset(2, xs, scale, record=full_att)
+    crops = [int(T * 0.25), int(np.floor(T * 0.95))]           # 512 and 1945 (9 valid in the tail block)
+    outs = {}
+    for seq, P in enumerate(crops):
+        xcont = dev(np.concatenate([x0[:P], xc[P:]]))
+        stack.replay(seq, xcont, scale)                           # contaminated run into the cache
+        assert stack.crop([seq], [P]) == 0
+        att = []
+        out = stack.replay(seq, xs[P:].contiguous(), scale, record=att)
+        assert stack.pool.seq_len(seq) == T
+        assert torch.equal(full[P:], out)                         # Theorem 1, bitwise
+        for a, fa in zip(att, full_att):
+            assert torch.equal(fa[P:], a)
+        outs[P] = (out, att)
+    log("oracle: 2 layers over 2048 tokens in fp64")
+    layers64 = [tuple(f32(m).astype(np.float64) for m in layer) for layer in ws]
+    ref_att = []
+    ref, _ = oracle.stacked_layers(f32(x0).astype(np.float64), layers64, geom.n_q_heads,
+                                   geom.n_kv_heads, geom.head_dim, scale, record=ref_att)
+    for P, (out, att) in outs.items():
+        for li, (a, ra) in enumerate(zip(att, ref_att)):
+            assert_close(_f64(a), ra[P:], "bf16", f"P={P}: attention output of layer {li}")
+        got, want = _f64(out), ref[P:]
+        d = np.abs(got - want)
+        log(f"P={P}: final state max|d| {d.max():.3e} (|ref| max {np.abs(want).max():.2f}), "
+            f"L1-rel {d.sum() / np.abs(want).sum():.3e}")
+        assert d.max() <= 2.0 ** -6 * np.abs(want).max()
+        assert d.sum() / np.abs(want).sum() <= 1e-2

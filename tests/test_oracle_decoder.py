@@ -46,6 +46,20 @@ def test_rms_norm():
     assert (DEC.rms_norm(np.zeros((1, 8)), np.ones(8), 1e-6) == 0).all()
 
 
+def test_rms_norm_eps_sits_inside_the_root():
+    """Hand value at eps != 0 (D2): x = [3, 4], g = 1, eps = 0.5 gives
+    mean(x^2) + eps = 12.5 + 0.5 = 13, so y = x / sqrt(13) exactly; eps added
+    after the root would give x / (sqrt(12.5) + 0.5) instead."""
+    y = DEC.rms_norm(np.array([[3.0, 4.0]]), np.ones(2), 0.5)
+    assert np.allclose(y, np.array([[3.0, 4.0]]) / np.sqrt(13.0), rtol=0, atol=1e-15)
+    assert not np.allclose(y, np.array([[3.0, 4.0]]) / (np.sqrt(12.5) + 0.5))
+    # the library routine with the same convention, at a large eps and a gain
+    rng = np.random.default_rng(3)
+    x, g = rng.standard_normal((4, 64)), rng.standard_normal(64)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (64,), torch.from_numpy(g), eps=0.75).numpy()
+    assert np.allclose(DEC.rms_norm(x, g, 0.75), ref, rtol=1e-12, atol=1e-14)
+
+
 def test_silu_matches_torch():
     g = np.linspace(-30, 30, 1001)
     assert np.allclose(DEC.silu(g), torch.nn.functional.silu(torch.from_numpy(g)).numpy(), rtol=1e-12,

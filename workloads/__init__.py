@@ -45,9 +45,20 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     Inputs drawn here are finite; NaN/inf are not produced by the generators.
     """
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    lsb = (u >> np.uint32(16)) & np.uint32(1)
-    rounded = u + np.uint32(0x7FFF) + lsb
-    return (rounded >> np.uint32(16)).astype(np.uint16)
+    flat = u.reshape(-1)
+    out = np.empty(flat.shape, np.uint16)
+    step = 1 << 20                      # in cache-sized pieces, one scratch buffer
+    tmp = np.empty(min(step, flat.size), np.uint32)
+    for i in range(0, flat.size, step):
+        src = flat[i:i + step]
+        t = tmp[:src.size]
+        np.right_shift(src, np.uint32(16), out=t)
+        np.bitwise_and(t, np.uint32(1), out=t)          # lsb of the kept half: ties to even
+        np.add(t, np.uint32(0x7FFF), out=t)
+        np.add(t, src, out=t)
+        np.right_shift(t, np.uint32(16), out=t)
+        out[i:i + src.size] = t
+    return out.reshape(u.shape)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
