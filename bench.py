@@ -145,6 +145,37 @@ class Setup:
                    for p, s in zip(self.P, self.S))
 
 
+def host_cpu() -> dict:
+    """The host the CPU baseline ran on: model name, sockets, physical cores
+    (distinct (socket, core) pairs in /proc/cpuinfo) and the logical CPUs this
+    process may use."""
+    model, pairs, logical = None, set(), 0
+    phys = core = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                key, _, val = line.partition(":")
+                key, val = key.strip(), val.strip()
+                if key == "processor":
+                    logical += 1
+                elif key == "model name" and model is None:
+                    model = val
+                elif key == "physical id":
+                    phys = val
+                elif key == "core id":
+                    core = val
+                elif not key and phys is not None:
+                    pairs.add((phys, core))
+                    phys = core = None
+        if phys is not None:
+            pairs.add((phys, core))
+    except OSError:
+        pass
+    sockets = len({p for p, _ in pairs}) or None
+    return {"cpu_model": model, "sockets": sockets, "physical_cores": len(pairs) or None,
+            "logical_cpus": logical or None, "usable_cpus": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(st: Setup, budget_s: float):
     """fp64 oracle on a bounded, evenly spaced sample of suffix tokens (all heads)."""
     import oracle
@@ -157,12 +188,15 @@ def cpu_baseline(st: Setup, budget_s: float):
     prepared = [(e, f64(e.q[e.prefix:]), f64(e.k), f64(e.v)) for e in st.eps]
     total_tokens = sum(st.S)
 
+    d = w.geometry.head_dim
+
     def run(frac):
         t0 = time.perf_counter()
-        n_done = 0
+        n_done, flop = 0, 0.0
         for e, q, k, v in prepared:
             n_tok = max(1, int(round(frac * e.suffix)))
             toks = np.linspace(0, e.suffix - 1, n_tok).round().astype(np.int64)
+            flop += 4.0 * d * hq * float(np.sum(e.prefix + toks + 1))   # QK^T and PV over keys <= p
             rows = (toks[:, None] * hq + np.arange(hq)[None, :]).reshape(-1)
             pool = oracle.PoolModel(2 * (e.t_contaminated // w.block_size + 2), 1,
                                     e.t_contaminated // w.block_size + 2, w.block_size)
@@ -171,14 +205,15 @@ def cpu_baseline(st: Setup, budget_s: float):
             pool.reserve([0], [e.suffix]); pool.commit([0], [e.suffix])
             oracle.attention(q, k, v, e.prefix, w.scale, rows=rows)
             n_done += n_tok
-        return n_done, time.perf_counter() - t0
+        return n_done, time.perf_counter() - t0, flop
 
-    n, dt = run(min(1.0, 64.0 / total_tokens))
+    n, dt, _ = run(min(1.0, 64.0 / total_tokens))
     frac = min(1.0, (n / total_tokens) * budget_s / max(dt, 1e-6))
-    n, dt = run(frac)
+    n, dt, flop = run(frac)
     return {"value": n / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
             "sample": f"{n} of {total_tokens} suffix tokens (evenly spaced in each episode, all "
-                      f"{hq} heads), fp64, {dt:.1f} s incl. crop + reserve on the oracle pool"}
+                      f"{hq} heads), fp64, {dt:.1f} s incl. crop + reserve on the oracle pool",
+            "fp64_gflops": flop / dt / 1e9, "threads": oracle.threads(), **host_cpu()}
 
 
 def bench_stack(args):
@@ -301,14 +336,6 @@ def measured_traffic(kernel_file: str, workload: str):
     the kernel source changed since the counters were taken."""
     rec = _profile_record(kernel_file, workload)
     return None if rec is None else rec["traffic_bytes_per_step"]
-
-
-def measured_sclk(kernel_file: str, workload: str):
-    """Mean shader clock (GHz) over the dominant kernel's dispatches in the
-    committed counter summary (GRBM_GUI_ACTIVE summed over the 8 XCDs, divided
-    by 8 and by the dispatch duration), or None."""
-    rec = _profile_record(kernel_file, workload)
-    return None if rec is None else rec.get("sclk_ghz")
 
 
 def copy_calibration(mib: int) -> None:
@@ -625,8 +652,12 @@ def main() -> int:
     # kernels' own dispatches (append, attention), an extra event splits off
     # the crop.  Kept out of the timed steps because issuing the instrumented
     # launches takes the host longer, which the GPU would wait for.
+    clk_cycles = clk_ticks = 0
+    clk_rate = None
     if single_call:
         pool.enable_timing(True)
+        if pipe:      # shader clock of the same dispatches, read in-kernel
+            pool.set_clock_probe(1 << 16)
         for i in range(args.steps):
             st.restore()
             torch.cuda.synchronize()
@@ -637,7 +668,13 @@ def main() -> int:
             a_ms, t_ms = pool.last_times()
             append_ms.append(a_ms)
             attn_ms.append(t_ms)
+            if pipe:
+                ghz, cyc, tck = pool.last_clock()
+                clk_cycles += cyc
+                clk_ticks += tck
+                clk_rate = ghz * tck / cyc          # reference ticks per ns
         pool.enable_timing(False)
+        pool.set_clock_probe(0)
     else:
         # kernel times per replay call, in a pass of its own (each call waits
         # for its events, which would stretch the timed steps)
@@ -670,7 +707,9 @@ def main() -> int:
     achieved = flops / (attn_mean * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     kfile = ("attn_bf16_pipe" if pipe else "attn_bf16") if w.dtype == "bf16" else "attn_f32"
-    sclk = measured_sclk(kfile, w.name)
+    # mean shader clock of the timed attention dispatches of this run (cycle and
+    # reference counters read by every workgroup at its start and end)
+    sclk = clk_cycles / clk_ticks * clk_rate if clk_ticks else None
     # crop: released table entries (each read, cleared, its count read and
     # written, then pushed) plus lengths and the stack top
     released = sum(-(-e.t_contaminated // w.block_size) - -(-e.prefix // w.block_size) for e in st.eps)
@@ -697,8 +736,9 @@ def main() -> int:
         "roofline": {"bound": "mfma" if w.dtype == "bf16" else "alu", "achieved": achieved,
                      "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": measured_traffic(kfile, w.name),
-                     # the clock the kernel actually ran at (counter summary) and the
-                     # fraction of the peak at that clock (peak scales with sclk / 2.4)
+                     # the clock the kernel ran at in this run's instrumented pass and
+                     # the fraction of the peak at that clock (peak scales with sclk / 2.4);
+                     # a diagnostic: frac is taken at the nominal 2.4 GHz
                      "sclk_ghz": sclk,
                      "frac_at_sclk": None if sclk is None else achieved / (peak * sclk / 2.4),
                      "kernel": ("attn_bf16_pipe_kernel<16>" if pipe

@@ -220,6 +220,23 @@ int pgsr_pool_enable_timing(pgsr_pool *pool, int on);
 int pgsr_pool_last_times(pgsr_pool *pool, float *append_ms, float *attention_ms);
 
 /*
+ * Shader-clock probe for profiling tools.  `buf` is caller-owned device memory
+ * of `bytes` bytes (NULL or 0 turns the probe off); it must outlive its use.
+ * While timing is on (pgsr_pool_enable_timing) and a buffer is set, a
+ * replay / full-reset call that runs the pipelined bf16 prefill kernel zeroes
+ * the buffer and then, for each of its first bytes / 32 workgroups, writes four
+ * uint64: the shader-cycle counter (s_memtime) and the constant-rate reference
+ * counter (s_memrealtime) at the workgroup's start and at its end.  A call
+ * with several attention launches keeps only its last one.
+ * pgsr_pool_last_clock waits for the stream, reads the buffer back and
+ * returns the mean shader clock over those workgroups in GHz (shader cycles
+ * over reference ticks times the reference rate), the summed cycles and the
+ * summed reference ticks; EINVAL when no timed launch wrote the probe.
+ */
+int pgsr_pool_set_clock_buffer(pgsr_pool *pool, void *buf, size_t bytes);
+int pgsr_pool_last_clock(pgsr_pool *pool, void *stream, double *ghz, int64_t *cycles, int64_t *ticks);
+
+/*
  * Choice of the bf16 prefill attention kernel (Algorithm 1 replay loop,
  * prefill form).  PGSR_PREFILL_AUTO (the default) runs the software-pipelined
  * kernel (two waves per SIMD, 32 query rows per wave) wherever it applies:

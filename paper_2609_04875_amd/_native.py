@@ -23,7 +23,7 @@ EXPORTS = (
     "pgsr_pool_refresh", "pgsr_seq_len", "pgsr_free_blocks", "pgsr_workspace_bytes",
     "pgsr_kv_crop", "pgsr_kv_fork", "pgsr_replay_prefill", "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
     "pgsr_pool_enable_timing", "pgsr_pool_last_times", "pgsr_pool_set_kv_scales",
-    "pgsr_pool_set_prefill_kernel",
+    "pgsr_pool_set_prefill_kernel", "pgsr_pool_set_clock_buffer", "pgsr_pool_last_clock",
     "pgsr_graph_create", "pgsr_graph_destroy", "pgsr_graph_append", "pgsr_graph_size",
     "pgsr_graph_session_length", "pgsr_graph_kv_length_after", "pgsr_graph_locate_source",
     "pgsr_graph_taint_closure", "pgsr_graph_policy_boundaries", "pgsr_ckpt_create",
@@ -90,6 +90,11 @@ def _load() -> ctypes.CDLL:
     lib.pgsr_pool_enable_timing.argtypes = [P, ctypes.c_int]
     lib.pgsr_pool_last_times.restype = ctypes.c_int
     lib.pgsr_pool_last_times.argtypes = [P, ctypes.POINTER(f32), ctypes.POINTER(f32)]
+    lib.pgsr_pool_set_clock_buffer.restype = ctypes.c_int
+    lib.pgsr_pool_set_clock_buffer.argtypes = [P, P, ctypes.c_size_t]
+    lib.pgsr_pool_last_clock.restype = ctypes.c_int
+    lib.pgsr_pool_last_clock.argtypes = [P, P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64),
+                                         ctypes.POINTER(i64)]
     lib.pgsr_pool_set_prefill_kernel.restype = ctypes.c_int
     lib.pgsr_pool_set_prefill_kernel.argtypes = [P, ctypes.c_int]
     lib.pgsr_gemm_bf16.restype = ctypes.c_int

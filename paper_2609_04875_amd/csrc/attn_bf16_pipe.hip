@@ -84,6 +84,11 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kPBuf][KT * KLD];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[kPBuf][D * VLD];
 
+  uint64_t clk0 = 0, rt0 = 0;
+  if (a.clk) {
+    clk0 = __builtin_amdgcn_s_memtime();
+    rt0 = __builtin_amdgcn_s_memrealtime();
+  }
   const int hkv = a.n_kv_heads;
   const int g = blockIdx.x % hkv;
   const int split = (blockIdx.x / hkv) % a.n_splits;
@@ -484,6 +489,14 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
           *(bf16x4*)(op + db * 32 + 8 * i4) = __builtin_convertvector(v4, bf16x4);
         }
     }
+  }
+  if (a.clk && tid == 0 && (int)blockIdx.x < a.clk_n) {
+    const uint64_t clk1 = __builtin_amdgcn_s_memtime(), rt1 = __builtin_amdgcn_s_memrealtime();
+    uint64_t* c = a.clk + 4 * (int64_t)blockIdx.x;
+    c[0] = clk0;
+    c[1] = clk1;
+    c[2] = rt0;
+    c[3] = rt1;
   }
 }
 

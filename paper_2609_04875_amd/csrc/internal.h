@@ -138,6 +138,10 @@ struct AttnArgs {
   int32_t row_begin, row_end;
   float* ws_acc;
   float* ws_ml;
+  // Clock probe (timing only, else null): workgroup b < clk_n writes
+  // {s_memtime at start, at end, s_memrealtime at start, at end} to clk[4b..].
+  uint64_t* clk;
+  int32_t clk_n;
   AttnEntry e[kMaxSeqsPerLaunch];
 };
 

@@ -46,6 +46,10 @@ struct pgsr_pool {
   // bf16 prefill kernel choice (PGSR_PREFILL_AUTO / PGSR_PREFILL_FOUR_WAVE)
   int prefill_kind = PGSR_PREFILL_AUTO;
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  // shader-clock probe (caller-owned device buffer, 4 uint64 per workgroup)
+  uint64_t* clk = nullptr;
+  int32_t clk_n = 0;
+  bool clk_written = false;
 };
 
 namespace {
@@ -419,6 +423,13 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
     }
+    if (p->timing && p->clk && pipe) {
+      hipError_t err = hipMemsetAsync(p->clk, 0, (size_t)p->clk_n * 4 * sizeof(uint64_t), st);
+      if (err != hipSuccess) return hip_fail(err, "clock probe reset");
+      a.clk = p->clk;
+      a.clk_n = p->clk_n;
+      p->clk_written = true;
+    }
     hipError_t err = p->dtype == PGSR_F32    ? launch_attn_f32(a, st)
                      : pipe                  ? launch_attn_bf16_pipe(a, st)
                      : p->dtype == PGSR_BF16 ? launch_attn_bf16(a, st)
@@ -588,6 +599,41 @@ int pgsr_pool_last_times(pgsr_pool* p, float* append_ms, float* attention_ms) {
   if (err == hipSuccess) err = hipEventElapsedTime(append_ms, p->ev[0], p->ev[1]);
   if (err == hipSuccess) err = hipEventElapsedTime(attention_ms, p->ev[2], p->ev[3]);
   if (err != hipSuccess) return hip_fail(err, "event timing");
+  return ok();
+}
+
+int pgsr_pool_set_clock_buffer(pgsr_pool* p, void* buf, size_t bytes) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  const size_t n = buf ? bytes / (4 * sizeof(uint64_t)) : 0;
+  p->clk = n ? (uint64_t*)buf : nullptr;
+  p->clk_n = (int32_t)std::min<size_t>(n, INT32_MAX);
+  p->clk_written = false;
+  return ok();
+}
+
+int pgsr_pool_last_clock(pgsr_pool* p, void* stream, double* ghz, int64_t* cycles, int64_t* ticks) {
+  if (!p || !ghz) return fail(PGSR_EINVAL, "null argument");
+  if (!p->clk || !p->clk_written) return fail(PGSR_EINVAL, "no timed launch wrote the clock probe");
+  std::vector<uint64_t> h((size_t)p->clk_n * 4);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t err = hipMemcpyAsync(h.data(), p->clk, h.size() * sizeof(uint64_t), hipMemcpyDeviceToHost, st);
+  if (err == hipSuccess) err = hipStreamSynchronize(st);
+  int dev = 0, khz = 0;
+  if (err == hipSuccess) err = hipGetDevice(&dev);
+  if (err == hipSuccess) err = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+  if (err != hipSuccess) return hip_fail(err, "clock probe read-back");
+  uint64_t cyc = 0, tck = 0;
+  for (int32_t b = 0; b < p->clk_n; ++b) {
+    const uint64_t* c = &h[4 * (size_t)b];
+    if (c[3] > c[2] && c[1] > c[0]) {
+      cyc += c[1] - c[0];
+      tck += c[3] - c[2];
+    }
+  }
+  if (tck == 0 || khz <= 0) return fail(PGSR_EINVAL, "the clock probe holds no workgroup");
+  *ghz = (double)cyc / (double)tck * (double)khz * 1e3 / 1e9;
+  if (cycles) *cycles = (int64_t)cyc;
+  if (ticks) *ticks = (int64_t)tck;
   return ok();
 }
 

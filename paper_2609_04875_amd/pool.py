@@ -138,6 +138,23 @@ class KVPool:
         N.check(N.lib.pgsr_pool_last_times(self._h, ctypes.byref(a), ctypes.byref(b)))
         return a.value, b.value
 
+    def set_clock_probe(self, workgroups: int = 0) -> None:
+        """Shader-clock probe on the bf16 prefill launches of timed calls: a
+        device buffer for ``workgroups`` workgroups (0 turns it off)."""
+        self._clk = (torch.zeros((max(workgroups, 0) * 4,), dtype=torch.int64, device=self.k_cache.device)
+                     if workgroups > 0 else None)
+        N.check(N.lib.pgsr_pool_set_clock_buffer(
+            self._h, self._clk.data_ptr() if self._clk is not None else None,
+            self._clk.numel() * 8 if self._clk is not None else 0))
+
+    def last_clock(self, stream=None):
+        """(GHz, shader cycles, reference ticks) summed over the workgroups of
+        the most recent timed prefill launch."""
+        ghz, cyc, tck = ctypes.c_double(), ctypes.c_int64(), ctypes.c_int64()
+        N.check(N.lib.pgsr_pool_last_clock(self._h, _stream_ptr(stream, self._dev), ctypes.byref(ghz),
+                                           ctypes.byref(cyc), ctypes.byref(tck)))
+        return ghz.value, cyc.value, tck.value
+
     # ---- the hot path ----
     def crop(self, seqs: Sequence[int], new_lens: Sequence[int], poison: bool = False,
              stream=None) -> int:
