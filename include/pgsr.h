@@ -199,6 +199,28 @@ int pgsr_replay_prefill(pgsr_pool *pool, int32_t layer, int32_t n, const int32_t
                         int64_t *recomputed_tokens, void *stream);
 
 /*
+ * pgsr_replay_prefill for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  Same arguments, kernels and results as pgsr_replay_prefill on
+ * a pool whose workspace were scratch_bytes large (bitwise), except that the
+ * split-key and decode partials live in a device array the library holds for
+ * the whole process on each GPU it runs on, PGSR_STATIC_SCRATCH_BYTES (64 MiB)
+ * large; the pool's own workspace is not used.  scratch_bytes bounds the
+ * partials of this call (pgsr_workspace_bytes sizes it: up to max_splits
+ * splits of up to max_total_q query tokens); 0 runs without splits;
+ * scratch_bytes > PGSR_STATIC_SCRATCH_BYTES is PGSR_ERANGE and changes
+ * nothing.  No hipMalloc, hipFree or other allocation of device memory.
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * there: calls whose work overlaps on one GPU (two streams, two host threads)
+ * race.  The partials need no clearing: each call writes every entry it reads.
+ */
+#define PGSR_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int pgsr_replay_prefill_static(pgsr_pool *pool, int32_t layer, int32_t n, const int32_t *seqs,
+                               const int32_t *q_lens, const void *q, const void *k, const void *v,
+                               void *o, float softmax_scale, unsigned flags, size_t scratch_bytes,
+                               int64_t *recomputed_tokens, void *stream);
+
+/*
  * Full reset (baseline B5, Section 4.1; T invocations of F, Corollary 1): on
  * layer 0 the sequences are first cropped to 0, then the whole sanitized
  * trajectory (lens[i] tokens) is replayed exactly as pgsr_replay_prefill does

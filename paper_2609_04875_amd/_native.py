@@ -15,13 +15,15 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("PGSR_LIB") or os.path.join(_PKG, "lib", "libpgsr.so")
 
 OK, EINVAL, ERANGE, ENOMEM, EUNSUPPORTED, EHIP, ENOENT = range(7)
+STATIC_SCRATCH_BYTES = 64 << 20      # PGSR_STATIC_SCRATCH_BYTES
 F32, BF16, FP8_E4M3 = 0, 1, 2
 COMMIT, POISON = 1, 2
 
 EXPORTS = (
     "pgsr_last_error", "pgsr_abi_version", "pgsr_pool_create", "pgsr_pool_destroy",
     "pgsr_pool_refresh", "pgsr_seq_len", "pgsr_free_blocks", "pgsr_workspace_bytes",
-    "pgsr_kv_crop", "pgsr_kv_fork", "pgsr_replay_prefill", "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
+    "pgsr_kv_crop", "pgsr_kv_fork", "pgsr_replay_prefill", "pgsr_replay_prefill_static",
+    "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
     "pgsr_pool_enable_timing", "pgsr_pool_last_times", "pgsr_pool_set_kv_scales",
     "pgsr_pool_set_prefill_kernel", "pgsr_pool_set_clock_buffer", "pgsr_pool_last_clock",
     "pgsr_graph_create", "pgsr_graph_destroy", "pgsr_graph_append", "pgsr_graph_size",
@@ -84,6 +86,9 @@ def _load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.restype = ctypes.c_int
         f.argtypes = [P, i32, i32, i32p, i32p, P, P, P, P, f32, u32, ctypes.POINTER(i64), P]
+    lib.pgsr_replay_prefill_static.restype = ctypes.c_int
+    lib.pgsr_replay_prefill_static.argtypes = [P, i32, i32, i32p, i32p, P, P, P, P, f32, u32, ctypes.c_size_t,
+                                               ctypes.POINTER(i64), P]
     lib.pgsr_pool_set_kv_scales.restype = ctypes.c_int
     lib.pgsr_pool_set_kv_scales.argtypes = [P, P, P]
     lib.pgsr_pool_enable_timing.restype = ctypes.c_int

@@ -9,6 +9,8 @@
 #include <cstddef>
 #include <cstdint>
 
+struct pgsr_pool;
+
 namespace pgsr {
 
 constexpr int kMaxSeqsPerLaunch = 64;
@@ -202,6 +204,15 @@ hipError_t launch_silu_mul(int32_t n, int32_t dff, const void* gu, void* out, hi
 // Text returned by pgsr_last_error() on this thread (host runtime).
 void set_error(const char* msg);
 void clear_error();
+// Sets the error text and returns code.
+int fail_with(int code, const char* msg);
+
+// pgsr_replay_prefill with an explicit split-key / decode workspace (the
+// pool's own, or the library's static scratch).
+int replay_prefill_ws(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+                      const int32_t* q_lens, const void* q, const void* k, const void* v, void* o,
+                      float softmax_scale, unsigned flags, int64_t* recomputed_tokens, void* ws,
+                      size_t ws_bytes, void* stream);
 
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s);

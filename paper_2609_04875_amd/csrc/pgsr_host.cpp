@@ -246,7 +246,9 @@ int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* se
 
 int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
               const int32_t* q_lens, const void* q, const void* k, const void* v, void* o,
-              float scale, unsigned flags, int64_t* recomputed, hipStream_t st) {
+              float scale, unsigned flags, int64_t* recomputed, void* ws, size_t ws_bytes,
+              hipStream_t st) {
+  if (ws == nullptr) ws_bytes = 0;
   // Segments with work, in call order (the packed inputs follow call order).
   std::vector<Seg> segs;
   segs.reserve(n);
@@ -333,7 +335,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
   const int group = p->hq / p->hkv;
   // Decode path: every sequence's queries fit one wave (32 / G tokens) and the
   // pool has a workspace (so batching already decides the rounding order).
-  bool decode = p->dtype != PGSR_F32 && p->workspace != nullptr;
+  bool decode = p->dtype != PGSR_F32 && ws_bytes > 0;
   for (const Seg& g : segs) decode = decode && g.q_len <= 32 / group;
   const bool pipe = p->dtype == PGSR_BF16 && p->prefill_kind == PGSR_PREFILL_AUTO &&
                     attn_bf16_pipe_eligible(p->d, group);
@@ -389,13 +391,13 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
       int64_t ns = (kDecodeTargetWaves + units - 1) / units;
       ns = std::min<int64_t>(ns, kDecodeMaxSplits);
       ns = std::min<int64_t>(ns, std::max<int64_t>(1, max_key / kDecodeMinSplitKeys));
-      ns = std::min<int64_t>(ns, (int64_t)(p->workspace_bytes / std::max<int64_t>(per_split, 1)));
+      ns = std::min<int64_t>(ns, (int64_t)(ws_bytes / std::max<int64_t>(per_split, 1)));
       if (ns > 1) {
         const int32_t kt = attn_decode_keys_per_tile();
         const int32_t len = cdiv(cdiv(max_key, ns), kt) * kt;
         a.n_splits = cdiv(max_key, len);
         a.split_len = len;
-        a.ws_acc = (float*)p->workspace;
+        a.ws_acc = (float*)ws;
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
       hipError_t err = launch_attn_decode(a, p->dtype == PGSR_FP8_E4M3, st);
@@ -409,17 +411,17 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     // fp32 kernel takes one query head per workgroup)
     const int64_t wgs = (int64_t)tiles * (p->dtype == PGSR_F32 ? p->hq : p->hkv);
     const int64_t target = pipe ? kSplitTargetWorkgroupsPipe : kSplitTargetWorkgroups;
-    if (p->workspace && wgs < target) {
+    if (ws_bytes > 0 && wgs < target) {
       int32_t max_key = 0;
       for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);
       const int64_t per_split = (int64_t)a.n_rows * ((int64_t)p->d + 2) * (int64_t)sizeof(float);
       int64_t ns = std::min<int64_t>(kMaxSplits, (target + wgs - 1) / wgs);
-      ns = std::min<int64_t>(ns, (int64_t)(p->workspace_bytes / std::max<int64_t>(per_split, 1)));
+      ns = std::min<int64_t>(ns, (int64_t)(ws_bytes / std::max<int64_t>(per_split, 1)));
       if (ns > 1) {
         const int32_t len = cdiv(cdiv(max_key, ns), kSplitAlign) * kSplitAlign;
         a.n_splits = cdiv(max_key, len);
         a.split_len = len;
-        a.ws_acc = (float*)p->workspace;
+        a.ws_acc = (float*)ws;
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
     }
@@ -760,6 +762,19 @@ int pgsr_replay_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* s
                         void* o, float softmax_scale, unsigned flags,
                         int64_t* recomputed_tokens, void* stream) {
   if (!p) return fail(PGSR_EINVAL, "pool is null");
+  return replay_prefill_ws(p, layer, n, seqs, q_lens, q, k, v, o, softmax_scale, flags,
+                           recomputed_tokens, p->workspace, p->workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace pgsr {
+
+int replay_prefill_ws(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+                      const int32_t* q_lens, const void* q, const void* k, const void* v, void* o,
+                      float softmax_scale, unsigned flags, int64_t* recomputed_tokens, void* ws,
+                      size_t ws_bytes, void* stream) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
   if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
   if (flags & ~(unsigned)PGSR_COMMIT) return fail(PGSR_EINVAL, "unknown replay flags 0x%x", flags);
   if (n > 0 && (!seqs || !q_lens)) return fail(PGSR_EINVAL, "null seqs / q_lens");
@@ -773,10 +788,16 @@ int pgsr_replay_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* s
   rc = check_replay(p, layer, n, seqs, q_lens, q, k, v, o, prefix, nalloc, p->h_top,
                     softmax_scale);
   if (rc) return rc;
-  rc = do_replay(p, layer, n, seqs, q_lens, q, k, v, o, softmax_scale, flags, recomputed_tokens,
-                 (hipStream_t)stream);
+  rc = do_replay(p, layer, n, seqs, q_lens, q, k, v, o, softmax_scale, flags, recomputed_tokens, ws,
+                 ws_bytes, (hipStream_t)stream);
   return rc ? rc : ok();
 }
+
+int fail_with(int code, const char* msg) { return fail(code, "%s", msg); }
+
+}  // namespace pgsr
+
+extern "C" {
 
 int pgsr_full_reset_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
                             const int32_t* lens, const void* q, const void* k, const void* v,
@@ -808,7 +829,8 @@ int pgsr_full_reset_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_
     rc = do_crop(p, n, seqs, zeros.data(), 0, st);
     if (rc) return rc;
   }
-  rc = do_replay(p, layer, n, seqs, lens, q, k, v, o, softmax_scale, flags, recomputed_tokens, st);
+  rc = do_replay(p, layer, n, seqs, lens, q, k, v, o, softmax_scale, flags, recomputed_tokens,
+                 p->workspace, p->workspace_bytes, st);
   return rc ? rc : ok();
 }
 

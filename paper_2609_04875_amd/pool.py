@@ -185,6 +185,16 @@ class KVPool:
         return self._prefill(N.lib.pgsr_replay_prefill, layer, seqs, q_lens, q, k, v, o, scale,
                              commit, stream)
 
+    def replay_static(self, layer: int, seqs, q_lens, q, k, v, o, scale: float, scratch_bytes: int,
+                      commit: bool = True, stream=None) -> int:
+        """``replay`` with the split / decode partials in the library's static
+        device scratch instead of the pool's workspace (no allocation), as if
+        the workspace were ``scratch_bytes`` large; returns the status."""
+        return self._prefill(
+            lambda h, layer_, n, s, ql, q_, k_, v_, o_, sc, fl, rec, st: N.lib.pgsr_replay_prefill_static(
+                h, layer_, n, s, ql, q_, k_, v_, o_, sc, fl, int(scratch_bytes), rec, st),
+            layer, seqs, q_lens, q, k, v, o, scale, commit, stream)
+
     def full_reset(self, layer: int, seqs, lens, q, k, v, o, scale: float, commit: bool = True,
                    stream=None) -> int:
         return self._prefill(N.lib.pgsr_full_reset_prefill, layer, seqs, lens, q, k, v, o, scale,
