@@ -5,7 +5,9 @@ must agree bit for bit; each must also meet the bf16 tolerance against the
 oracle.  Cases cover every group size the pipelined kernel takes, block sizes
 16 / 32 / 64, crops not aligned to a block with NaN-poisoned tail slots,
 suffixes shorter than one query tile, tiles that straddle the diagonal, and
-several sequences of different lengths in one call."""
+several sequences of different lengths in one call; then the default kernel
+on more shapes against the oracle and against the full reset of every
+sequence in one call (bitwise)."""
 import numpy as np
 import pytest
 import torch
@@ -67,6 +69,54 @@ def test_pipelined_equals_four_wave_and_oracle(hq, hkv, B, ps):
     for e, a, b in zip(eps, pipe, four):
         assert torch.equal(a, b), f"pipelined and four-wave kernels differ (P={e.prefix}, S={e.suffix})"
         assert_close(a.float().cpu().numpy(), oracle_suffix(e, scale), "bf16", f"P={e.prefix} S={e.suffix}")
+
+
+# the default kernel on more shapes: the 8B replay at full size, one partial
+# query tile, tiles that straddle the diagonal, every group size dividing 16
+DEFAULT_CASES = [
+    (32, 8, 16, [(8189, 2048)]),         # the 8B replay at full size
+    (32, 8, 16, [(300, 31)]),            # one partial query tile
+    (32, 8, 16, [(0, 64)]),              # one tile, prefix 0
+    (32, 8, 16, [(77, 96)]),             # a tile and a partial one
+    (32, 8, 32, [(1000, 130)]),          # B = 32
+    (16, 16, 64, [(129, 300)]),          # G = 1, B = 64
+    (16, 8, 16, [(50, 150)]),            # G = 2
+    (64, 8, 16, [(700, 45)]),            # G = 8
+    (64, 4, 16, [(65, 37)]),             # G = 16
+    (32, 8, 16, [(517, 90), (0, 33), (2000, 257), (63, 1), (4000, 700)]),   # ragged batch
+]
+
+
+@pytest.mark.parametrize("hq,hkv,B,ps", DEFAULT_CASES)
+def test_default_kernel_matches_oracle_and_full_reset(hq, hkv, B, ps):
+    geom = W.AttnGeometry(hq, hkv, 128)
+    log(f"default kernel {hq}/{hkv} B={B} episodes {ps}")
+    rng = np.random.default_rng(hq * 131 + B + sum(p + 3 * s for p, s in ps))
+    eps = [W.draw_episode(rng, geom, "bf16", P, S, P + S + 3) for P, S in ps]
+    scale = 128 ** -0.5
+    outs = _run("auto", geom, eps, B, scale)
+    for e, o in zip(eps, outs):
+        if e.suffix * hq <= 65536:
+            ref, rows = oracle_suffix(e, scale), None
+            got = o.float().cpu().numpy()
+        else:                                # the full-size case: every 7th row
+            rows = np.arange(0, e.suffix * hq, 7)
+            ref = oracle_suffix(e, scale, rows=rows)
+            got = o.reshape(-1, 128)[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+        assert_close(got, ref, "bf16", f"P={e.prefix} S={e.suffix}")
+    # Theorem 1, bitwise: the full reset of each sanitized trajectory in one call
+    nb = sum(_blocks(e.t_sanitized, B) for e in eps) + 4
+    mbps = max(_blocks(e.t_sanitized, B) for e in eps) + 2
+    pool = make_pool(geom, "bf16", nb, len(eps), mbps, block_size=B)
+    fq, fk, fv = (torch.cat([dev(getattr(e, x), "bf16") for e in eps]) for x in ("q", "k", "v"))
+    fo = torch.empty_like(fq)
+    assert pool.full_reset(0, list(range(len(eps))), [e.t_sanitized for e in eps], fq, fk, fv, fo,
+                           scale) == 0
+    torch.cuda.synchronize()
+    off = 0
+    for e, o in zip(eps, outs):
+        assert torch.equal(fo[off + e.prefix:off + e.t_sanitized], o), f"P={e.prefix} S={e.suffix}"
+        off += e.t_sanitized
 
 
 def test_pipelined_full_reset_equals_replay_at_8b_crop():
