@@ -109,26 +109,42 @@ class Setup:
         self.pool.load_meta(self.saved)
 
     def step(self, ev=None) -> None:
-        """crop + replay; optional events: ev[0] start, ev[1] after crop (None:
-        not recorded), ev[2] end."""
+        """Restore (crop) + replay: one restore + replay call for the first (or
+        only) replay call of the step, plain replay calls for the remaining
+        chunks; optional events ev[0] at the start, ev[1] at the end."""
         torch = self.torch
         s = torch.cuda.current_stream()
         if ev:
             ev[0].record(s)
-        if self.pool.crop(self.seqs, self.P):
-            raise RuntimeError("crop failed")
-        if ev and ev[1] is not None:
-            ev[1].record(s)
         if self.chunk:
             for c0 in range(0, self.S[0], self.chunk):
                 sl = slice(c0, c0 + self.chunk)
-                if self.pool.replay(0, [0], [self.chunk], self.q[sl], self.k[sl], self.v[sl],
-                                    self.o[sl], self.w.scale):
+                args = ([0], [self.chunk], self.q[sl], self.k[sl], self.v[sl], self.o[sl], self.w.scale)
+                rc = (self.pool.restore_replay(0, args[0], self.P, *args[1:]) if c0 == 0
+                      else self.pool.replay(0, *args))
+                if rc:
                     raise RuntimeError("replay failed")
-        elif self.pool.replay(0, self.seqs, self.S, self.q, self.k, self.v, self.o, self.w.scale):
-            raise RuntimeError("replay failed")
+        elif self.pool.restore_replay(0, self.seqs, self.P, self.S, self.q, self.k, self.v, self.o,
+                                      self.w.scale):
+            raise RuntimeError("restore + replay failed")
         if ev:
-            ev[2].record(s)
+            ev[1].record(s)
+
+    def crop_call_ms(self, reps: int) -> list:
+        """Latency of the crop call alone (HIP events around it), after a restore."""
+        torch = self.torch
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        out = []
+        for _ in range(reps):
+            self.restore()
+            torch.cuda.synchronize()
+            ev[0].record()
+            if self.pool.crop(self.seqs, self.P):
+                raise RuntimeError("crop failed")
+            ev[1].record()
+            torch.cuda.synchronize()
+            out.append(ev[0].elapsed_time(ev[1]))
+        return out
 
     def flops(self) -> float:
         g = self.w.geometry
@@ -637,21 +653,21 @@ def main() -> int:
     pipe = (w.dtype == "bf16" and args.prefill_kernel == "auto" and g.head_dim == 128
             and 32 % (g.n_q_heads // g.n_kv_heads) == 0)
     single_call = st.calls_per_step == 1
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    step_ms, crop_ms, attn_ms, append_ms, inst_ms = [], [], [], [], []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    step_ms, attn_ms, append_ms, inst_ms = [], [], [], []
     # Timed steps: nothing but the step's own launches between the two events.
     pool.enable_timing(False)
     for i in range(args.warmup + args.steps):
         st.restore()                          # outside the timed region
         torch.cuda.synchronize()
-        st.step([ev[0], None, ev[2]])
+        st.step(ev)
         torch.cuda.synchronize()
         if i >= args.warmup:
-            step_ms.append(ev[0].elapsed_time(ev[2]))
+            step_ms.append(ev[0].elapsed_time(ev[1]))
     # The same K steps again, instrumented: the library's events ride on its
-    # kernels' own dispatches (append, attention), an extra event splits off
-    # the crop.  Kept out of the timed steps because issuing the instrumented
-    # launches takes the host longer, which the GPU would wait for.
+    # kernels' own dispatches (the append launch, which carries the crop, and
+    # the attention).  Kept out of the timed steps because issuing the
+    # instrumented launches takes the host longer, which the GPU would wait for.
     clk_cycles = clk_ticks = 0
     clk_rate = None
     if single_call:
@@ -663,8 +679,7 @@ def main() -> int:
             torch.cuda.synchronize()
             st.step(ev)
             torch.cuda.synchronize()
-            crop_ms.append(ev[0].elapsed_time(ev[1]))
-            inst_ms.append(ev[0].elapsed_time(ev[2]))
+            inst_ms.append(ev[0].elapsed_time(ev[1]))
             a_ms, t_ms = pool.last_times()
             append_ms.append(a_ms)
             attn_ms.append(t_ms)
@@ -682,21 +697,21 @@ def main() -> int:
         for _ in range(3):
             st.restore()
             torch.cuda.synchronize()
-            ev[0].record()
-            pool.crop(st.seqs, st.P)
-            ev[1].record()
-            torch.cuda.synchronize()
-            crop_ms.append(ev[0].elapsed_time(ev[1]))
             a_tot = t_tot = 0.0
             for c0 in range(0, st.S[0], st.chunk):
                 sl = slice(c0, c0 + st.chunk)
-                pool.replay(0, [0], [st.chunk], st.q[sl], st.k[sl], st.v[sl], st.o[sl], w.scale)
+                if c0 == 0:
+                    pool.restore_replay(0, [0], st.P, [st.chunk], st.q[sl], st.k[sl], st.v[sl], st.o[sl],
+                                        w.scale)
+                else:
+                    pool.replay(0, [0], [st.chunk], st.q[sl], st.k[sl], st.v[sl], st.o[sl], w.scale)
                 a_ms, t_ms = pool.last_times()
                 a_tot += a_ms
                 t_tot += t_ms
             append_ms.append(a_tot)
             attn_ms.append(t_tot)
         pool.enable_timing(False)
+    crop_ms = st.crop_call_ms(5)             # the crop as a call of its own, for its latency
     if args.calibrate_copy_mib:
         copy_calibration(args.calibrate_copy_mib)
 
@@ -749,7 +764,8 @@ def main() -> int:
                      "algorithmic_GBps": nbytes / (attn_mean * 1e-3) / 1e9},
         "crop": {"us": float(np.mean(crop_ms)) * 1e3, "algorithmic_bytes": crop_bytes,
                  "released_blocks": released},
-        "breakdown_ms": {"crop": float(np.mean(crop_ms)), "append": float(np.mean(append_ms)),
+        "breakdown_ms": {"crop_call": float(np.mean(crop_ms)),
+                         "restore_append": float(np.mean(append_ms)),
                          "attention": attn_mean, "step": total_s * 1e3 / args.steps,
                          "step_min": float(np.min(step_ms)),
                          "step_instrumented": float(np.mean(inst_ms)) if inst_ms else None},

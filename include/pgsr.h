@@ -199,6 +199,25 @@ int pgsr_replay_prefill(pgsr_pool *pool, int32_t layer, int32_t n, const int32_t
                         int64_t *recomputed_tokens, void *stream);
 
 /*
+ * Algorithm 1's restore step followed by the first layer of its replay loop,
+ * in one call (Section 3.4 (b): restoring a checkpoint is a crop; Theorem 1:
+ * replay from there).  The same device state, outputs and recompute count,
+ * bit for bit, as pgsr_kv_crop(pool, n, seqs, restore_lens, 0, stream)
+ * followed by pgsr_replay_prefill(pool, layer, n, seqs, q_lens, ...), but
+ * validated together on the host mirror (all-or-nothing across both: the
+ * replay is checked against the state the crop leaves) and, where it applies
+ * (bf16 pool, at most 16 sequences each with query tokens, at most 512
+ * appended blocks, no kept partial tail block shared with another row), with
+ * the crop's device work in the append launch: one launch and one host call
+ * fewer between the restore and the replay.  seqs, restore_lens, q_lens: HOST
+ * arrays of n; the other arguments as for pgsr_replay_prefill.
+ */
+int pgsr_restore_replay_prefill(pgsr_pool *pool, int32_t layer, int32_t n, const int32_t *seqs,
+                                const int32_t *restore_lens, const int32_t *q_lens, const void *q,
+                                const void *k, const void *v, void *o, float softmax_scale,
+                                unsigned flags, int64_t *recomputed_tokens, void *stream);
+
+/*
  * pgsr_replay_prefill for callers that cannot allocate device memory: code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation.  Same arguments, kernels and results as pgsr_replay_prefill on

@@ -23,6 +23,7 @@ EXPORTS = (
     "pgsr_last_error", "pgsr_abi_version", "pgsr_pool_create", "pgsr_pool_destroy",
     "pgsr_pool_refresh", "pgsr_seq_len", "pgsr_free_blocks", "pgsr_workspace_bytes",
     "pgsr_kv_crop", "pgsr_kv_fork", "pgsr_replay_prefill", "pgsr_replay_prefill_static",
+    "pgsr_restore_replay_prefill",
     "pgsr_full_reset_prefill", "pgsr_gemm_bf16",
     "pgsr_pool_enable_timing", "pgsr_pool_last_times", "pgsr_pool_set_kv_scales",
     "pgsr_pool_set_prefill_kernel", "pgsr_pool_set_clock_buffer", "pgsr_pool_last_clock",
@@ -86,6 +87,9 @@ def _load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.restype = ctypes.c_int
         f.argtypes = [P, i32, i32, i32p, i32p, P, P, P, P, f32, u32, ctypes.POINTER(i64), P]
+    lib.pgsr_restore_replay_prefill.restype = ctypes.c_int
+    lib.pgsr_restore_replay_prefill.argtypes = [P, i32, i32, i32p, i32p, i32p, P, P, P, P, f32, u32,
+                                                ctypes.POINTER(i64), P]
     lib.pgsr_replay_prefill_static.restype = ctypes.c_int
     lib.pgsr_replay_prefill_static.argtypes = [P, i32, i32, i32p, i32p, P, P, P, P, f32, u32, ctypes.c_size_t,
                                                ctypes.POINTER(i64), P]

@@ -106,6 +106,37 @@ struct AppendArgs {
   AppendEntry e[kMaxSeqsPerLaunch];
 };
 
+// Restore + reserve + append in one launch (bf16 pools, no copy-on-write, no
+// poisoning): workgroup (0, 0) takes the crop of `ce` exactly as crop_kernel
+// does, then the reservation pops of `e` from the stack it just pushed to
+// (tables, counts, lengths, top); the other workgroups copy the K/V of item
+// blockIdx.x - 1 and KV head blockIdx.y into block ids[item], which the host
+// mirror computed by the same steps.
+constexpr int kMaxFusedSeqs = 16;
+constexpr int kMaxFusedItems = 512;
+
+struct FusedAppendArgs {
+  void* k_cache;
+  void* v_cache;
+  const void* k_in;
+  const void* v_in;
+  int32_t* tables;
+  int32_t* lens;
+  int32_t* free_list;
+  int32_t* free_top;
+  int32_t* refs;
+  int32_t max_bps, n_blocks, n_kv_heads, block_size, head_dim, layer;
+  int32_t commit;
+  int32_t top_before;  // stack height before the crop
+  int32_t top_after;   // after the reservation
+  int32_t n_crop;
+  int32_t n;
+  int32_t n_items;
+  CropEntry ce[kMaxFusedSeqs];
+  AppendEntry e[kMaxFusedSeqs];
+  int32_t ids[kMaxFusedItems];
+};
+
 // -------------------------------------------------------------- attention - //
 struct AttnEntry {
   int32_t seq;
@@ -174,6 +205,10 @@ hipError_t launch_crop(const CropArgs& a, hipStream_t s);
 hipError_t launch_poison(const PoisonArgs& a, hipStream_t s);
 hipError_t launch_fork(const ForkArgs& a, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s);
+// False when the fused launch does not cover this geometry (the caller then
+// launches crop and append separately).
+bool fused_append_supported(int block_size, int head_dim);
+hipError_t launch_fused_append(const FusedAppendArgs& a, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 // Software-pipelined bf16 prefill for head_dim 128 and GQA groups dividing

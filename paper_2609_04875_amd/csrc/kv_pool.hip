@@ -269,6 +269,213 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
   }
 }
 
+// K/V of the tokens of one (sequence, logical block) item for one KV head,
+// bf16 pools, one wave: tokens p0 .. p0+nt-1 (block slots s0 .. s0+nt-1) from
+// the packed inputs (rows of n_kv_heads * D elements) into the block-head at
+// kc (K, [slot][d]) and vc (V, [d][slot]).  Every lane issues all of its loads
+// (up to four 16-byte chunks of K and four of V per round) before any store;
+// V is staged [slot][d] in LDS (rows padded to D + 8) and written back along d
+// rows: 16-byte runs of 8 slots when the span starts and ends on 8-slot
+// boundaries, else slot by slot (the partial first and last blocks).
+template <int B, int D>
+__device__ inline void copy_block_head(const uint16_t* __restrict__ kin, const uint16_t* __restrict__ vin,
+                                       int64_t row_stride, uint16_t* __restrict__ kc,
+                                       uint16_t* __restrict__ vc, int s0, int nt, uint16_t* vstage) {
+  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+  constexpr int C8 = D / 8, DP = D + 8;
+  const int lane = threadIdx.x;
+  const int nck = nt * C8;                   // 16-byte chunks of K (and of V) here
+  if (nt == B && B * C8 <= 4 * 64) {         // a whole block in one round, constant indices
+    u4 kk[B * C8 / 64], vv[B * C8 / 64];
+#pragma unroll
+    for (int j = 0; j < B * C8 / 64; ++j) {
+      const int i = j * 64 + lane;
+      const int64_t off = (i / C8) * row_stride + (i % C8) * 8;
+      kk[j] = *(const u4*)(kin + off);
+      vv[j] = *(const u4*)(vin + off);
+    }
+#pragma unroll
+    for (int j = 0; j < B * C8 / 64; ++j) {
+      const int i = j * 64 + lane, t = i / C8, c = (i % C8) * 8;
+      *(u4*)(kc + (int64_t)t * D + c) = kk[j];
+      *(u4*)(&vstage[t * DP + c]) = vv[j];
+    }
+  }
+  for (int i0 = 0; i0 < nck && !(nt == B && B * C8 <= 4 * 64); i0 += 4 * 64) {
+    u4 kk[4], vv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = i0 + j * 64 + lane;
+      if (i < nck) {
+        const int64_t off = (i / C8) * row_stride + (i % C8) * 8;
+        kk[j] = *(const u4*)(kin + off);
+        vv[j] = *(const u4*)(vin + off);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = i0 + j * 64 + lane;
+      if (i < nck) {
+        const int t = i / C8, c = (i % C8) * 8;
+        *(u4*)(kc + (int64_t)(s0 + t) * D + c) = kk[j];
+        *(u4*)(&vstage[t * DP + c]) = vv[j];
+      }
+    }
+  }
+  __syncthreads();
+  if (nt == B) {                             // a whole block: constant trip counts
+    constexpr int S8 = B / 8;
+#pragma unroll
+    for (int i = lane; i < D * S8; i += 64) {
+      const int d = i / S8, t0 = (i % S8) * 8;
+      u4 out;
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        out[w] = (uint32_t)vstage[(t0 + 2 * w) * DP + d] | ((uint32_t)vstage[(t0 + 2 * w + 1) * DP + d] << 16);
+      *(u4*)(vc + (int64_t)d * B + t0) = out;
+    }
+  } else if ((s0 & 7) == 0 && (nt & 7) == 0) {
+    const int S8 = nt / 8;
+    for (int i = lane; i < D * S8; i += 64) {
+      const int d = i / S8, t0 = (i % S8) * 8;
+      u4 out;
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        out[w] = (uint32_t)vstage[(t0 + 2 * w) * DP + d] | ((uint32_t)vstage[(t0 + 2 * w + 1) * DP + d] << 16);
+      *(u4*)(vc + (int64_t)d * B + s0 + t0) = out;
+    }
+  } else {
+    // a partial first or last block: slot by slot, lanes along d (no division
+    // by the run length; these two items per sequence set the launch's length)
+    for (int t = 0; t < nt; ++t)
+#pragma unroll
+      for (int d = lane; d < D; d += 64) vc[(int64_t)d * B + s0 + t] = vstage[t * DP + d];
+  }
+}
+
+// Reserve + append for bf16 pools: one wave per (sequence, logical block) item
+// and KV head; block ids read from the table or straight from the stack
+// (free_list[stack_before - 1 - k] for the k-th new block of the sequence), so
+// no workgroup depends on another's table write.
+template <int B, int D>
+__global__ void __launch_bounds__(64) append_bf16_kernel(AppendArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t vstage[B * (D + 8)];
+  const int item = blockIdx.x, lane = threadIdx.x;
+  int ei = 0;
+  while (ei + 1 < a.n && a.e[ei + 1].item_start <= item) ++ei;
+  const AppendEntry e = a.e[ei];
+  const int h = blockIdx.y;
+  const int32_t lb = e.lb_first + (item - e.item_start);
+  const int32_t p0 = max(e.prefix, lb * B);
+  const int32_t p1 = min(e.prefix + e.q_len, (lb + 1) * B);
+  int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
+  const int32_t cow_pops = e.cow_old >= 0 ? 1 : 0;   // cow_kernel took the first pop
+  const int32_t id = lb < e.nalloc_before
+                         ? row[lb]
+                         : a.free_list[e.stack_before - 1 - cow_pops - (lb - e.nalloc_before)];
+  if (h == 0 && lane == 0) {
+    if (lb >= e.nalloc_before) {
+      row[lb] = id;
+      a.refs[id] = 1;
+    }
+    if (a.commit && item == e.item_start) a.lens[e.seq] = e.prefix + e.q_len;
+    if (a.write_top && item == 0) *a.free_top = a.top_after;
+  }
+  const int64_t row_stride = (int64_t)a.n_kv_heads * D;
+  const int64_t src0 = ((int64_t)(e.q_off + (p0 - e.prefix)) * a.n_kv_heads + h) * D;
+  const int64_t blk = ((int64_t)a.layer * a.n_blocks + id) * a.n_kv_heads + h;
+  copy_block_head<B, D>((const uint16_t*)a.k_in + src0, (const uint16_t*)a.v_in + src0, row_stride,
+                        (uint16_t*)a.k_cache + blk * B * D, (uint16_t*)a.v_cache + blk * D * B,
+                        p0 - lb * B, p1 - p0, vstage);
+}
+
+// Restore + reserve + append in one launch.  Workgroup (0, 0) runs the crop of
+// a.ce in call order (released entries of a row, 256 at a time: -1 into the
+// table, count decremented, blocks reaching 0 pushed in ascending order by
+// ballot prefix counts), then the reservation of a.e in call order (the k-th
+// new block of an entry is free_list[stack_before - 1 - k] of the stack the
+// crop just left, named in the table with count 1), then the lengths and the
+// stack top; its accesses are ordered by the barriers between rounds.  Every
+// other workgroup copies one item's K/V for one KV head into ids[item] and
+// touches no metadata.
+template <int B, int D>
+__global__ void __launch_bounds__(64) fused_append_kernel(FusedAppendArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t vstage[B * (D + 8)];
+  const int lane = threadIdx.x, h = blockIdx.y;
+  if (blockIdx.x == 0) {
+    if (h != 0) return;
+    // 256 entries per round, entry j0 + 64 r + lane in lane's slot r, so the
+    // ascending push order is r-major: position = pushes of slots before r
+    // plus pushes of lower lanes in slot r.
+    constexpr int R = 4;
+    const uint64_t below = (1ull << lane) - 1ull;
+    int32_t top = a.top_before;
+    for (int i = 0; i < a.n_crop; ++i) {
+      const CropEntry c = a.ce[i];
+      int32_t* row = a.tables + (int64_t)c.seq * a.max_bps;
+      for (int32_t j0 = c.keep; j0 < c.nalloc; j0 += R * 64) {
+        int32_t b[R], r[R];
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          const int32_t j = j0 + 64 * k + lane;
+          b[k] = j < c.nalloc ? row[j] : -1;
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k) r[k] = b[k] >= 0 ? a.refs[b[k]] - 1 : 1;
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          const int32_t j = j0 + 64 * k + lane;
+          if (b[k] >= 0) {
+            row[j] = -1;
+            a.refs[b[k]] = r[k];
+          }
+          const uint64_t m = __ballot(r[k] == 0);
+          if (r[k] == 0) a.free_list[top + __popcll(m & below)] = b[k];
+          top += __popcll(m);
+        }
+        __syncthreads();   // this round's table, count and stack writes precede the next round's reads
+      }
+      if (lane == 0) a.lens[c.seq] = c.new_len;
+    }
+    for (int i = 0; i < a.n; ++i) {
+      const AppendEntry e = a.e[i];
+      int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
+      const int32_t end = (e.prefix + e.q_len + B - 1) / B;
+      for (int32_t lb0 = e.nalloc_before; lb0 < end; lb0 += R * 64) {
+        int32_t id[R];
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          const int32_t lb = lb0 + 64 * k + lane;
+          id[k] = lb < end ? a.free_list[e.stack_before - 1 - (lb - e.nalloc_before)] : -1;
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+          if (id[k] >= 0) {
+            row[lb0 + 64 * k + lane] = id[k];
+            a.refs[id[k]] = 1;
+          }
+        }
+      }
+      if (lane == 0 && a.commit) a.lens[e.seq] = e.prefix + e.q_len;
+    }
+    if (lane == 0) *a.free_top = a.top_after;
+    return;
+  }
+  const int item = blockIdx.x - 1;
+  int ei = 0;
+  while (ei + 1 < a.n && a.e[ei + 1].item_start <= item) ++ei;
+  const AppendEntry e = a.e[ei];
+  const int32_t lb = e.lb_first + (item - e.item_start);
+  const int32_t p0 = max(e.prefix, lb * B);
+  const int32_t p1 = min(e.prefix + e.q_len, (lb + 1) * B);
+  const int64_t row_stride = (int64_t)a.n_kv_heads * D;
+  const int64_t src0 = ((int64_t)(e.q_off + (p0 - e.prefix)) * a.n_kv_heads + h) * D;
+  const int64_t blk = ((int64_t)a.layer * a.n_blocks + a.ids[item]) * a.n_kv_heads + h;
+  copy_block_head<B, D>((const uint16_t*)a.k_in + src0, (const uint16_t*)a.v_in + src0, row_stride,
+                        (uint16_t*)a.k_cache + blk * B * D, (uint16_t*)a.v_cache + blk * D * B,
+                        p0 - lb * B, p1 - p0, vstage);
+}
+
 }  // namespace
 
 hipError_t launch_pool_init(int32_t* tables, int64_t n_table, int32_t* lens, int32_t max_seqs,
@@ -318,12 +525,42 @@ hipError_t launch_append(const AppendArgs& a, int elem_bytes, hipStream_t s) {
     hipLaunchKernelGGL((append_kernel<uint32_t, uint32_t>), grid, dim3(256), 0, s, a);
   } else if (elem_bytes == 2) {
     if (any_cow) hipLaunchKernelGGL(cow_kernel<uint16_t>, cow_grid, dim3(256), 0, s, a);
-    hipLaunchKernelGGL((append_kernel<uint16_t, uint16_t>), grid, dim3(256), 0, s, a);
+    if (a.head_dim == 128 && a.block_size == 16)
+      hipLaunchKernelGGL((append_bf16_kernel<16, 128>), grid, dim3(64), 0, s, a);
+    else if (a.head_dim == 128 && a.block_size == 32)
+      hipLaunchKernelGGL((append_bf16_kernel<32, 128>), grid, dim3(64), 0, s, a);
+    else if (a.head_dim == 128 && a.block_size == 64)
+      hipLaunchKernelGGL((append_bf16_kernel<64, 128>), grid, dim3(64), 0, s, a);
+    else if (a.head_dim == 64 && a.block_size == 16)
+      hipLaunchKernelGGL((append_bf16_kernel<16, 64>), grid, dim3(64), 0, s, a);
+    else if (a.head_dim == 64 && a.block_size == 32)
+      hipLaunchKernelGGL((append_bf16_kernel<32, 64>), grid, dim3(64), 0, s, a);
+    else if (a.head_dim == 64 && a.block_size == 64)
+      hipLaunchKernelGGL((append_bf16_kernel<64, 64>), grid, dim3(64), 0, s, a);
+    else
+      hipLaunchKernelGGL((append_kernel<uint16_t, uint16_t>), grid, dim3(256), 0, s, a);
   } else {                                          // FP8 cache, bf16 inputs
     if (any_cow) hipLaunchKernelGGL(cow_kernel<uint8_t>, cow_grid, dim3(256), 0, s, a);
     hipLaunchKernelGGL((append_kernel<uint16_t, uint8_t>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
+}
+
+bool fused_append_supported(int block_size, int head_dim) {
+  return (head_dim == 128 || head_dim == 64) && (block_size == 16 || block_size == 32 || block_size == 64);
+}
+
+hipError_t launch_fused_append(const FusedAppendArgs& a, hipStream_t s) {
+  const dim3 grid(1 + a.n_items, a.n_kv_heads);
+#define PGSR_FUSED(BS, HD)                                                                      \
+  if (a.block_size == BS && a.head_dim == HD) {                                                  \
+    hipLaunchKernelGGL((fused_append_kernel<BS, HD>), grid, dim3(64), 0, s, a);                  \
+    return hipGetLastError();                                                                    \
+  }
+  PGSR_FUSED(16, 128) PGSR_FUSED(32, 128) PGSR_FUSED(64, 128)
+  PGSR_FUSED(16, 64) PGSR_FUSED(32, 64) PGSR_FUSED(64, 64)
+#undef PGSR_FUSED
+  return hipErrorInvalidValue;
 }
 
 }  // namespace pgsr

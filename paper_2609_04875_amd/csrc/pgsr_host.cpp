@@ -79,15 +79,22 @@ inline int32_t cdiv(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
 
 int elem_bytes(const pgsr_pool* p) { return p->dtype == PGSR_F32 ? 4 : p->dtype == PGSR_BF16 ? 2 : 1; }
 
-// Distinct, in-range sequence ids.
+// Distinct, in-range sequence ids (a pairwise check for the few sequences of
+// a typical call, a table past that).
 int check_seqs(const pgsr_pool* p, int32_t n, const int32_t* seqs) {
+  for (int32_t i = 0; i < n; ++i)
+    if (seqs[i] < 0 || seqs[i] >= p->max_seqs)
+      return fail(PGSR_EINVAL, "sequence id %d outside [0, %d)", seqs[i], p->max_seqs);
+  if (n <= 32) {
+    for (int32_t i = 0; i < n; ++i)
+      for (int32_t j = 0; j < i; ++j)
+        if (seqs[i] == seqs[j]) return fail(PGSR_EINVAL, "sequence id %d appears twice in one call", seqs[i]);
+    return PGSR_OK;
+  }
   std::vector<char> seen(p->max_seqs, 0);
   for (int32_t i = 0; i < n; ++i) {
-    const int32_t s = seqs[i];
-    if (s < 0 || s >= p->max_seqs)
-      return fail(PGSR_EINVAL, "sequence id %d outside [0, %d)", s, p->max_seqs);
-    if (seen[s]) return fail(PGSR_EINVAL, "sequence id %d appears twice in one call", s);
-    seen[s] = 1;
+    if (seen[seqs[i]]) return fail(PGSR_EINVAL, "sequence id %d appears twice in one call", seqs[i]);
+    seen[seqs[i]] = 1;
   }
   return PGSR_OK;
 }
@@ -109,6 +116,20 @@ void mirror_crop(pgsr_pool* p, int32_t s, int32_t L) {
 
 // Blocks a crop of these sequences would push (the mirror is left unchanged).
 int64_t count_freed(const pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_lens) {
+  // without sharing (every released block named once) each release frees its block
+  int64_t released = 0;
+  bool shared = false;
+  for (int32_t i = 0; i < n && !shared; ++i) {
+    const int32_t s = seqs[i], keep = cdiv(new_lens[i], p->B);
+    for (int32_t j = keep; j < p->h_nalloc[s]; ++j) {
+      if (p->h_ref[p->h_tab[(size_t)s * p->max_bps + j]] != 1) {
+        shared = true;
+        break;
+      }
+      ++released;
+    }
+  }
+  if (!shared) return released;
   std::unordered_map<int32_t, int32_t> dec;   // block -> decrements so far
   int64_t freed = 0;
   for (int32_t i = 0; i < n; ++i) {
@@ -244,10 +265,18 @@ int check_replay(const pgsr_pool* p, int32_t layer, int32_t n, const int32_t* se
   return PGSR_OK;
 }
 
+// A crop whose device work rides in the replay's append launch: its entries
+// (mirror already updated) and the stack height before it.
+struct FoldedCrop {
+  int32_t n = 0;
+  int32_t top_before = 0;
+  CropEntry e[kMaxFusedSeqs];
+};
+
 int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
               const int32_t* q_lens, const void* q, const void* k, const void* v, void* o,
               float scale, unsigned flags, int64_t* recomputed, void* ws, size_t ws_bytes,
-              hipStream_t st) {
+              hipStream_t st, const FoldedCrop* fold = nullptr) {
   if (ws == nullptr) ws_bytes = 0;
   // Segments with work, in call order (the packed inputs follow call order).
   std::vector<Seg> segs;
@@ -265,8 +294,61 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     hipError_t err = hipEventRecord(p->ev[0], st);
     if (err != hipSuccess) return hip_fail(err, "timing event");
   }
+  // Restore + reserve + append in one launch (the caller checked that it
+  // applies); the mirror takes the same pops in call order and records each
+  // item's block for the copying workgroups.
+  if (fold) {
+    FusedAppendArgs a{};
+    a.k_cache = p->k_cache;
+    a.v_cache = p->v_cache;
+    a.k_in = k;
+    a.v_in = v;
+    a.tables = p->tables;
+    a.lens = p->lens;
+    a.free_list = p->free_list;
+    a.free_top = p->free_top;
+    a.refs = p->refs;
+    a.max_bps = p->max_bps;
+    a.n_blocks = p->n_blocks;
+    a.n_kv_heads = p->hkv;
+    a.block_size = p->B;
+    a.head_dim = p->d;
+    a.layer = layer;
+    a.commit = commit ? 1 : 0;
+    a.top_before = fold->top_before;
+    a.n_crop = fold->n;
+    std::memcpy(a.ce, fold->e, sizeof(CropEntry) * fold->n);
+    a.n = (int32_t)segs.size();
+    int32_t items = 0;
+    for (int32_t i = 0; i < a.n; ++i) {
+      const Seg& g = segs[i];
+      AppendEntry& e = a.e[i];
+      int32_t* row = &p->h_tab[(size_t)g.seq * p->max_bps];
+      e.seq = g.seq;
+      e.prefix = g.prefix;
+      e.q_len = g.q_len;
+      e.q_off = g.q_off;
+      e.nalloc_before = p->h_nalloc[g.seq];
+      e.stack_before = p->h_top;
+      e.lb_first = g.prefix / p->B;
+      e.item_start = items;
+      e.cow_old = -1;
+      const int32_t end_blocks = cdiv((int64_t)g.prefix + g.q_len, p->B);
+      for (int32_t lb = p->h_nalloc[g.seq]; lb < end_blocks; ++lb) {
+        const int32_t nb = p->h_free[--p->h_top];
+        p->h_ref[nb] = 1;
+        row[lb] = nb;
+      }
+      p->h_nalloc[g.seq] = std::max(p->h_nalloc[g.seq], end_blocks);
+      for (int32_t lb = e.lb_first; lb < end_blocks; ++lb) a.ids[items++] = row[lb];
+    }
+    a.n_items = items;
+    a.top_after = p->h_top;
+    hipError_t err = launch_fused_append(a, st);
+    if (err != hipSuccess) return hip_fail(err, "restore + append launch");
+  }
   // Reserve + append, chunked; the mirror takes the same pops in call order.
-  for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
+  for (size_t base = 0; !fold && base < segs.size(); base += kMaxSeqsPerLaunch) {
     const int32_t cnt = (int32_t)std::min<size_t>(kMaxSeqsPerLaunch, segs.size() - base);
     AppendArgs a{};
     a.k_cache = p->k_cache;
@@ -454,6 +536,73 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     if (recomputed) *recomputed += total;
   }
   return PGSR_OK;
+}
+
+// Restore (crop seqs[i] to crop_lens[i]; none when crop_lens is null) then the
+// replay of q_lens on `layer`, validated together on the mirror before anything
+// is launched.  The crop's device work rides in the append launch when that
+// launch covers it: a bf16 pool with a fused kernel for its geometry, at most
+// kMaxFusedSeqs sequences and kMaxFusedItems appended blocks, every sequence
+// with work, and no kept partial tail block named by another row (so no
+// copy-on-write).  Otherwise the crop is its own launch first.
+int restore_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+                   const int32_t* crop_lens, const int32_t* q_lens, const void* q, const void* k,
+                   const void* v, void* o, float scale, unsigned flags, int64_t* recomputed,
+                   hipStream_t st) {
+  int rc = check_seqs(p, n, seqs);
+  if (rc) return rc;
+  std::vector<int32_t> prefix(n), nalloc(n);
+  int64_t free_after = p->h_top;
+  if (crop_lens) {
+    for (int32_t i = 0; i < n; ++i) {
+      const int32_t L = crop_lens[i], len = p->h_len[seqs[i]];
+      if (L < 0 || L > len)
+        return fail(PGSR_ERANGE, "crop of sequence %d to %d tokens; it holds %d", seqs[i], L, len);
+    }
+    free_after += count_freed(p, n, seqs, crop_lens);
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    prefix[i] = crop_lens ? crop_lens[i] : p->h_len[seqs[i]];
+    nalloc[i] = crop_lens ? cdiv(crop_lens[i], p->B) : p->h_nalloc[seqs[i]];
+  }
+  rc = check_replay(p, layer, n, seqs, q_lens, q, k, v, o, prefix, nalloc, (int32_t)free_after, scale);
+  if (rc) return rc;
+  if (!crop_lens || n == 0)
+    return do_replay(p, layer, n, seqs, q_lens, q, k, v, o, scale, flags, recomputed, p->workspace,
+                     p->workspace_bytes, st);
+  bool fold = p->dtype == PGSR_BF16 && fused_append_supported(p->B, p->d) && n <= kMaxFusedSeqs;
+  int64_t items = 0;
+  for (int32_t i = 0; fold && i < n; ++i) {
+    const int32_t L = crop_lens[i], S = q_lens[i];
+    if (S <= 0) fold = false;
+    items += cdiv((int64_t)L + S, p->B) - L / p->B;
+    if (L % p->B != 0) {   // the kept partial tail block must be this row's alone
+      const int32_t b = p->h_tab[(size_t)seqs[i] * p->max_bps + L / p->B];
+      if (b < 0 || p->h_ref[b] != 1) fold = false;
+    }
+  }
+  if (items > kMaxFusedItems) fold = false;
+  if (!fold) {
+    rc = do_crop(p, n, seqs, crop_lens, 0, st);
+    if (rc) return rc;
+    return do_replay(p, layer, n, seqs, q_lens, q, k, v, o, scale, flags, recomputed, p->workspace,
+                     p->workspace_bytes, st);
+  }
+  FoldedCrop fc;
+  fc.n = n;
+  fc.top_before = p->h_top;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = seqs[i], L = crop_lens[i];
+    CropEntry& e = fc.e[i];
+    e.seq = s;
+    e.new_len = L;
+    e.keep = cdiv(L, p->B);
+    e.nalloc = p->h_nalloc[s];
+    mirror_crop(p, s, L);
+    e.tail_private = 0;
+  }
+  return do_replay(p, layer, n, seqs, q_lens, q, k, v, o, scale, flags, recomputed, p->workspace,
+                   p->workspace_bytes, st, &fc);
 }
 
 }  // namespace
@@ -807,30 +956,23 @@ int pgsr_full_reset_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_
   if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
   if (flags & ~(unsigned)PGSR_COMMIT) return fail(PGSR_EINVAL, "unknown replay flags 0x%x", flags);
   if (n > 0 && (!seqs || !lens)) return fail(PGSR_EINVAL, "null seqs / lens");
-  int rc = check_seqs(p, n, seqs);
-  if (rc) return rc;
-  // Validate the replay as it will run after the crop (prefix 0, rows emptied).
-  std::vector<int32_t> prefix(n), nalloc(n), zeros(n, 0);
-  int32_t free_after = p->h_top + (layer == 0 ? (int32_t)count_freed(p, n, seqs, zeros.data()) : 0);
-  for (int32_t i = 0; i < n; ++i) {
-    if (layer == 0) {
-      prefix[i] = 0;
-      nalloc[i] = 0;
-    } else {
-      prefix[i] = p->h_len[seqs[i]];
-      nalloc[i] = p->h_nalloc[seqs[i]];
-    }
-  }
-  rc = check_replay(p, layer, n, seqs, lens, q, k, v, o, prefix, nalloc, free_after,
-                    softmax_scale);
-  if (rc) return rc;
-  hipStream_t st = (hipStream_t)stream;
-  if (layer == 0 && n > 0) {
-    rc = do_crop(p, n, seqs, zeros.data(), 0, st);
-    if (rc) return rc;
-  }
-  rc = do_replay(p, layer, n, seqs, lens, q, k, v, o, softmax_scale, flags, recomputed_tokens,
-                 p->workspace, p->workspace_bytes, st);
+  // layer 0: restore every sequence to 0 tokens, then replay the whole trajectory
+  std::vector<int32_t> zeros(n, 0);
+  const int rc = restore_replay(p, layer, n, seqs, layer == 0 ? zeros.data() : nullptr, lens, q, k, v, o,
+                                softmax_scale, flags, recomputed_tokens, (hipStream_t)stream);
+  return rc ? rc : ok();
+}
+
+int pgsr_restore_replay_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
+                                const int32_t* restore_lens, const int32_t* q_lens, const void* q,
+                                const void* k, const void* v, void* o, float softmax_scale,
+                                unsigned flags, int64_t* recomputed_tokens, void* stream) {
+  if (!p) return fail(PGSR_EINVAL, "pool is null");
+  if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
+  if (flags & ~(unsigned)PGSR_COMMIT) return fail(PGSR_EINVAL, "unknown replay flags 0x%x", flags);
+  if (n > 0 && (!seqs || !restore_lens || !q_lens)) return fail(PGSR_EINVAL, "null seqs / lens");
+  const int rc = restore_replay(p, layer, n, seqs, restore_lens, q_lens, q, k, v, o, softmax_scale,
+                                flags, recomputed_tokens, (hipStream_t)stream);
   return rc ? rc : ok();
 }
 

@@ -185,6 +185,19 @@ class KVPool:
         return self._prefill(N.lib.pgsr_replay_prefill, layer, seqs, q_lens, q, k, v, o, scale,
                              commit, stream)
 
+    def restore_replay(self, layer: int, seqs, restore_lens, q_lens, q, k, v, o, scale: float,
+                       commit: bool = True, stream=None) -> int:
+        """Restore (crop to ``restore_lens``) then replay ``q_lens`` tokens on
+        ``layer``, in one call: the same result as ``crop`` then ``replay``,
+        all-or-nothing across both; returns the status."""
+        if len(restore_lens) != len(seqs):
+            raise ValueError(f"{len(seqs)} sequences but {len(restore_lens)} restore lengths")
+        rl = N.int32_array(restore_lens)
+        return self._prefill(
+            lambda h, layer_, n, s, ql, q_, k_, v_, o_, sc, fl, rec, st: N.lib.pgsr_restore_replay_prefill(
+                h, layer_, n, s, rl, ql, q_, k_, v_, o_, sc, fl, rec, st),
+            layer, seqs, q_lens, q, k, v, o, scale, commit, stream)
+
     def replay_static(self, layer: int, seqs, q_lens, q, k, v, o, scale: float, scratch_bytes: int,
                       commit: bool = True, stream=None) -> int:
         """``replay`` with the split / decode partials in the library's static

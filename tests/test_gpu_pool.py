@@ -2,6 +2,8 @@
 model: block tables, lengths, free-list stack and stack height bit-exact after
 every call (Algorithm 1 restore and replay steps; Section 3.4 (b)), appended
 K/V bits exact, kept prefix untouched (Lemma 1), errors change nothing."""
+import copy
+
 import numpy as np
 import pytest
 import torch
@@ -37,7 +39,34 @@ def test_random_crop_replay_trace_matches_oracle(dtype, B, seed):
     expect_v = [x.copy() for x in expect_k]
     _compare(pool, model, "init")
     for step in range(40):
-        if rng.random() < 0.45:
+        if rng.random() < 0.3:
+            # restore + replay in one call: the oracle's crop then reservation,
+            # all-or-nothing across both
+            seqs = rng.choice(n_seqs, size=int(rng.integers(1, 4)), replace=False).tolist()
+            new = [int(rng.integers(0, model.lens[s] + 1)) for s in seqs]
+            if rng.random() < 0.1:                       # an invalid crop: nothing may change
+                new[0] = int(model.lens[seqs[0]]) + 1
+            q_lens = [int(rng.integers(1, 3 * B)) for _ in seqs]
+            tot = sum(q_lens)
+            q = W.round_to_dtype(rng.standard_normal((tot, GEOM.n_q_heads, GEOM.head_dim)).astype(np.float32), dtype)
+            k = W.round_to_dtype(rng.standard_normal((tot, GEOM.n_kv_heads, GEOM.head_dim)).astype(np.float32), dtype)
+            v = W.round_to_dtype(rng.standard_normal((tot, GEOM.n_kv_heads, GEOM.head_dim)).astype(np.float32), dtype)
+            o = torch.empty((tot, GEOM.n_q_heads, GEOM.head_dim), dtype=pool.dtype, device="cuda")
+            trial = copy.deepcopy(model)
+            want = trial.crop(seqs, new)
+            if want == 0:
+                want = trial.reserve(seqs, q_lens)
+            got = pool.restore_replay(0, seqs, new, q_lens, dev(q, dtype), dev(k, dtype), dev(v, dtype), o, 0.125)
+            assert got == want, (step, got, want)
+            if want == 0:
+                trial.commit(seqs, q_lens)
+                model = trial
+                off = 0
+                for s_, L, S in zip(seqs, new, q_lens):
+                    expect_k[s_] = np.concatenate([expect_k[s_][:L], k[off:off + S]])
+                    expect_v[s_] = np.concatenate([expect_v[s_][:L], v[off:off + S]])
+                    off += S
+        elif rng.random() < 0.45:
             seqs = rng.choice(n_seqs, size=int(rng.integers(1, 4)), replace=False).tolist()
             new = [int(rng.integers(0, model.lens[s] + 1)) for s in seqs]
             if rng.random() < 0.1:                       # an invalid crop: nothing may change
@@ -152,3 +181,43 @@ def test_poisoned_slots_are_never_read():
     got = o.float().cpu().numpy()
     assert np.isfinite(got).all()
     assert_close(got, oracle_suffix(ep, 128 ** -0.5), "bf16", "poisoned replay")
+
+
+@pytest.mark.parametrize("P,S,Tc,B", [(8189, 2048, 10240, 16), (300, 77, 420, 32), (64, 200, 300, 64)])
+def test_restore_replay_equals_crop_then_replay(P, S, Tc, B):
+    """One call for Algorithm 1's restore and the first replay layer (the crop
+    folded into the append launch) against the two separate calls: identical
+    tables, lengths, stack, counts, cached K/V and outputs, bit for bit."""
+    from gpu_helpers import oracle_suffix, assert_close
+    geom = W.AttnGeometry(32, 8, 128)
+    rng = np.random.default_rng(P + S)
+    ep = W.draw_episode(rng, geom, "bf16", P, S, Tc)
+    scale = 128 ** -0.5
+    nb = -(-Tc // B) + -(-(P + S) // B) + 8
+    mbps = -(-max(Tc, P + S) // B) + 2
+    outs, states, kvs = [], [], []
+    for fused in (True, False):
+        log(f"restore + replay P={P} S={S} B={B} fused={fused}")
+        pool = make_pool(geom, "bf16", nb, 1, mbps, block_size=B)
+        cq, ck, cv = (dev(ep.contaminated(x), "bf16") for x in ("q", "k", "v"))
+        assert pool.replay(0, [0], [Tc], cq, ck, cv, torch.empty_like(cq), scale) == 0
+        q, k, v = (dev(getattr(ep, x)[P:], "bf16") for x in ("q", "k", "v"))
+        o = torch.empty_like(q)
+        before = pool.recomputed_tokens.value
+        if fused:
+            assert pool.restore_replay(0, [0], [P], [S], q, k, v, o, scale) == 0
+        else:
+            assert pool.crop([0], [P]) == 0
+            assert pool.replay(0, [0], [S], q, k, v, o, scale) == 0
+        assert pool.recomputed_tokens.value - before == S
+        outs.append(o)
+        states.append(pool.state())
+        kvs.append(logical_kv(pool, 0, 0, P + S))
+    for key in states[0]:
+        assert np.array_equal(np.asarray(states[0][key]), np.asarray(states[1][key])), key
+    assert torch.equal(kvs[0][0], kvs[1][0]) and torch.equal(kvs[0][1], kvs[1][1])
+    assert torch.equal(outs[0], outs[1])
+    rows = np.arange(0, S * 32, 97)
+    ref = oracle_suffix(ep, scale, rows=rows)
+    got = outs[0].reshape(-1, 128)[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    assert_close(got, ref, "bf16", "restore + replay")
