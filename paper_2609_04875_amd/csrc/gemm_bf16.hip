@@ -66,35 +66,37 @@ gemm_bf16_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
   // Loads read clamped (always valid) addresses, so the load sequence has no
   // branches: rows past M or N only feed output rows and columns that are
   // never stored, and chunks past K are zeroed when they are written to LDS.
-  u32x4 xr[CPX], wr[CPW];
-  auto load = [&](int k0) {
+  // Two register sets of staged chunks: the loads for K step kt+2 are issued
+  // while step kt is multiplied, so each has two steps of products to arrive.
+  u32x4 xr[2][CPX], wr[2][CPW];
+  auto load = [&](int set, int k0) {
 #pragma unroll
     for (int i = 0; i < CPX; ++i) {
       const int c = tid + i * NT;
       const int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
-      xr[i] = *(const u32x4*)(X + (int64_t)min(m0 + row, M - 1) * K + min(k0 + kc, K - 8));
+      xr[set][i] = *(const u32x4*)(X + (int64_t)min(m0 + row, M - 1) * K + min(k0 + kc, K - 8));
     }
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
       const int c = tid + i * NT;
       const int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
-      wr[i] = *(const u32x4*)(W + (int64_t)min(n0 + row, N - 1) * K + min(k0 + kc, K - 8));
+      wr[set][i] = *(const u32x4*)(W + (int64_t)min(n0 + row, N - 1) * K + min(k0 + kc, K - 8));
     }
   };
-  auto store = [&](int buf, int k0) {
+  auto store = [&](int set, int buf, int k0) {
     const bool tail = k0 + BK > K;
 #pragma unroll
     for (int i = 0; i < CPX; ++i) {
       const int c = tid + i * NT;
       const int kc = (c % (BK / 8)) * 8;
-      const u32x4 v = tail && k0 + kc >= K ? u32x4{0, 0, 0, 0} : xr[i];
+      const u32x4 v = tail && k0 + kc >= K ? u32x4{0, 0, 0, 0} : xr[set][i];
       *(u32x4*)&xs[buf][(c / (BK / 8)) * LDK + kc] = v;
     }
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
       const int c = tid + i * NT;
       const int kc = (c % (BK / 8)) * 8;
-      const u32x4 v = tail && k0 + kc >= K ? u32x4{0, 0, 0, 0} : wr[i];
+      const u32x4 v = tail && k0 + kc >= K ? u32x4{0, 0, 0, 0} : wr[set][i];
       *(u32x4*)&ws[buf][(c / (BK / 8)) * LDK + kc] = v;
     }
   };
@@ -106,12 +108,7 @@ gemm_bf16_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x16{};
 
   const int nk = (K + BK - 1) / BK;
-  load(0);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    store(buf, kt * BK);        // buffer last read two steps ago, one barrier before
-    if (kt + 1 < nk) load((kt + 1) * BK);
-    __syncthreads();
+  auto mma = [&](int buf) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       bf16x8 wa[TN], xb[TM];
@@ -129,7 +126,24 @@ gemm_bf16_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
         for (int j = 0; j < TM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[i], xb[j], acc[i][j], 0, 0, 0);
     }
+  };
+  // step kt: its chunks (register set kt % 2) go to LDS buffer kt % 2, last
+  // read two steps ago with a barrier since; then step kt+2 is requested
+  // into the same register set and step kt is multiplied.
+  auto kstep = [&](int set, int kt) {
+    store(set, set, kt * BK);
+    if (kt + 2 < nk) load(set, (kt + 2) * BK);
+    __syncthreads();
+    mma(set);
+  };
+  load(0, 0);
+  if (nk > 1) load(1, BK);
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    kstep(0, kt);
+    kstep(1, kt + 1);
   }
+  if (kt < nk) kstep(0, kt);
   // acc[i][j] lane (r, hh), register q: n = wn + 32i + 8(q/4) + 4hh + q%4,
   // m = wm + 32j + r.
 #pragma unroll
