@@ -625,8 +625,9 @@ def main() -> int:
     ap.add_argument("--workload", default=DEFAULT)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--prefill-kernel", choices=("auto", "four_wave"), default="auto",
-                    help="bf16 prefill kernel: pipelined where it applies (auto) or four-wave")
+    ap.add_argument("--prefill-kernel", choices=("auto", "pipelined", "four_wave"), default="auto",
+                    help="bf16 prefill kernel: wide, else pipelined, where they apply (auto); "
+                         "never the wide kernel (pipelined); four-wave")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device (counter scaling)")
     args = ap.parse_args()
@@ -650,8 +651,11 @@ def main() -> int:
     st = Setup(args.workload)
     w, g, pool = st.w, st.w.geometry, st.pool
     pool.set_prefill_kernel(args.prefill_kernel)
-    pipe = (w.dtype == "bf16" and args.prefill_kernel == "auto" and g.head_dim == 128
-            and 32 % (g.n_q_heads // g.n_kv_heads) == 0)
+    # which bf16 prefill kernel the library runs (the host's selection rule)
+    fast = (w.dtype == "bf16" and g.head_dim == 128 and 32 % (g.n_q_heads // g.n_kv_heads) == 0)
+    wide = (fast and args.prefill_kernel == "auto" and w.block_size == 16
+            and pool.n_blocks * g.n_kv_heads * 4096 <= 1 << 32)
+    pipe = fast and not wide and args.prefill_kernel in ("auto", "pipelined")
     single_call = st.calls_per_step == 1
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     step_ms, attn_ms, append_ms, inst_ms = [], [], [], []
@@ -672,7 +676,7 @@ def main() -> int:
     clk_rate = None
     if single_call:
         pool.enable_timing(True)
-        if pipe:      # shader clock of the same dispatches, read in-kernel
+        if wide or pipe:      # shader clock of the same dispatches, read in-kernel
             pool.set_clock_probe(1 << 16)
         for i in range(args.steps):
             st.restore()
@@ -683,7 +687,7 @@ def main() -> int:
             a_ms, t_ms = pool.last_times()
             append_ms.append(a_ms)
             attn_ms.append(t_ms)
-            if pipe:
+            if wide or pipe:
                 ghz, cyc, tck = pool.last_clock()
                 clk_cycles += cyc
                 clk_ticks += tck
@@ -721,7 +725,8 @@ def main() -> int:
     attn_mean = float(np.mean(attn_ms))
     achieved = flops / (attn_mean * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
-    kfile = ("attn_bf16_pipe" if pipe else "attn_bf16") if w.dtype == "bf16" else "attn_f32"
+    kfile = (("attn_bf16_wide" if wide else "attn_bf16_pipe" if pipe else "attn_bf16")
+             if w.dtype == "bf16" else "attn_f32")
     # mean shader clock of the timed attention dispatches of this run (cycle and
     # reference counters read by every workgroup at its start and end)
     sclk = clk_cycles / clk_ticks * clk_rate if clk_ticks else None
@@ -756,7 +761,8 @@ def main() -> int:
                      # a diagnostic: frac is taken at the nominal 2.4 GHz
                      "sclk_ghz": sclk,
                      "frac_at_sclk": None if sclk is None else achieved / (peak * sclk / 2.4),
-                     "kernel": ("attn_bf16_pipe_kernel<16>" if pipe
+                     "kernel": ("attn_bf16_wide_kernel" if wide
+                                else "attn_bf16_pipe_kernel<16>" if pipe
                                 else f"attn_bf16_kernel<{g.head_dim},4,16>" if w.dtype == "bf16"
                                 else f"attn_f32_kernel<{g.head_dim}>"),
                      "flops_per_step": flops, "algorithmic_bytes_per_step": nbytes,

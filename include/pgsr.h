@@ -279,14 +279,17 @@ int pgsr_pool_last_clock(pgsr_pool *pool, void *stream, double *ghz, int64_t *cy
 
 /*
  * Choice of the bf16 prefill attention kernel (Algorithm 1 replay loop,
- * prefill form).  PGSR_PREFILL_AUTO (the default) runs the software-pipelined
- * kernel (two waves per SIMD, 32 query rows per wave) wherever it applies:
- * head_dim 128, a GQA group dividing 32, a bf16 pool; every other call runs
- * the four-wave kernel.  PGSR_PREFILL_FOUR_WAVE runs the four-wave kernel for
- * every call.  Both give identical bits for every query row; the option only
- * moves time.  Host only, no device work; EINVAL for another value.
+ * prefill form).  PGSR_PREFILL_AUTO (the default) runs, for a bf16 pool with
+ * head_dim 128 and a GQA group dividing 32, the wide kernel (one wave per
+ * SIMD, 64 query rows per wave, global->LDS tile loads) when the pool has
+ * 16-token blocks and n_blocks * n_kv_heads * 4 KB <= 4 GB, else the
+ * software-pipelined kernel (two waves per SIMD, 32 query rows per wave);
+ * every other call runs the four-wave kernel.  PGSR_PREFILL_PIPELINED skips
+ * the wide kernel; PGSR_PREFILL_FOUR_WAVE runs the four-wave kernel for every
+ * call.  All give identical bits for every query row; the option only moves
+ * time.  Host only, no device work; EINVAL for another value.
  */
-enum { PGSR_PREFILL_AUTO = 0, PGSR_PREFILL_FOUR_WAVE = 1 };
+enum { PGSR_PREFILL_AUTO = 0, PGSR_PREFILL_FOUR_WAVE = 1, PGSR_PREFILL_PIPELINED = 2 };
 int pgsr_pool_set_prefill_kernel(pgsr_pool *pool, int kind);
 
 /*

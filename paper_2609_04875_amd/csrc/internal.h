@@ -212,10 +212,15 @@ hipError_t launch_fused_append(const FusedAppendArgs& a, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 // Software-pipelined bf16 prefill for head_dim 128 and GQA groups dividing
-// 32: one wave per SIMD, 64 query rows per wave, one workgroup per CU.
+// 32: two waves per SIMD, 32 query rows per wave, one workgroup per CU.
 bool attn_bf16_pipe_eligible(int head_dim, int group);
 int attn_bf16_pipe_tile_tokens(int group);
 hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s);
+// The same tiles and bits with one wave per SIMD holding 64 query rows and
+// global->LDS tile loads: 16-token blocks, pools whose layer-head block range
+// fits 32-bit byte offsets.  Tile tokens as attn_bf16_pipe_tile_tokens.
+bool attn_bf16_wide_eligible(int head_dim, int group, int block_size, int64_t n_blocks, int n_kv_heads);
+hipError_t launch_attn_bf16_wide(const AttnArgs& a, hipStream_t s);
 // Same kernel over an FP8 E4M3 cache: codes widen to bf16 exactly on the way
 // into LDS; the K scale is in scale_log2, the V scale in o_scale.
 hipError_t launch_attn_fp8(const AttnArgs& a, hipStream_t s);

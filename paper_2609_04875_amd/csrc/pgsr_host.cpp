@@ -43,7 +43,7 @@ struct pgsr_pool {
   bool timing = false, timed_call = false;
   // FP8 pools: per-layer K and V scales (stored code = x / scale, read = code * scale)
   std::vector<float> k_scale, v_scale;
-  // bf16 prefill kernel choice (PGSR_PREFILL_AUTO / PGSR_PREFILL_FOUR_WAVE)
+  // bf16 prefill kernel choice (PGSR_PREFILL_AUTO / _FOUR_WAVE / _PIPELINED)
   int prefill_kind = PGSR_PREFILL_AUTO;
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   // shader-clock probe (caller-owned device buffer, 4 uint64 per workgroup)
@@ -419,10 +419,13 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
   // pool has a workspace (so batching already decides the rounding order).
   bool decode = p->dtype != PGSR_F32 && ws_bytes > 0;
   for (const Seg& g : segs) decode = decode && g.q_len <= 32 / group;
-  const bool pipe = p->dtype == PGSR_BF16 && p->prefill_kind == PGSR_PREFILL_AUTO &&
+  const bool wide = p->dtype == PGSR_BF16 && p->prefill_kind == PGSR_PREFILL_AUTO &&
+                    attn_bf16_wide_eligible(p->d, group, p->B, p->n_blocks, p->hkv);
+  const bool pipe = !wide && p->dtype == PGSR_BF16 &&
+                    (p->prefill_kind == PGSR_PREFILL_AUTO || p->prefill_kind == PGSR_PREFILL_PIPELINED) &&
                     attn_bf16_pipe_eligible(p->d, group);
   const int tile_tokens = p->dtype == PGSR_F32 ? attn_f32_tile_tokens(p->d, group)
-                          : pipe               ? attn_bf16_pipe_tile_tokens(group)
+                          : wide || pipe       ? attn_bf16_pipe_tile_tokens(group)
                                                : attn_bf16_tile_tokens(p->d, group);
   for (size_t base = 0; base < segs.size(); base += kMaxSeqsPerLaunch) {
     const int32_t cnt = (int32_t)std::min<size_t>(kMaxSeqsPerLaunch, segs.size() - base);
@@ -492,7 +495,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     // (the bf16 kernel packs a KV head's query heads into one workgroup, the
     // fp32 kernel takes one query head per workgroup)
     const int64_t wgs = (int64_t)tiles * (p->dtype == PGSR_F32 ? p->hq : p->hkv);
-    const int64_t target = pipe ? kSplitTargetWorkgroupsPipe : kSplitTargetWorkgroups;
+    const int64_t target = wide || pipe ? kSplitTargetWorkgroupsPipe : kSplitTargetWorkgroups;
     if (ws_bytes > 0 && wgs < target) {
       int32_t max_key = 0;
       for (int32_t i = 0; i < cnt; ++i) max_key = std::max(max_key, chunk[i].prefix + chunk[i].q_len);
@@ -507,7 +510,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
         a.ws_ml = a.ws_acc + (int64_t)a.n_splits * a.n_rows * p->d;
       }
     }
-    if (p->timing && p->clk && pipe) {
+    if (p->timing && p->clk && (wide || pipe)) {
       hipError_t err = hipMemsetAsync(p->clk, 0, (size_t)p->clk_n * 4 * sizeof(uint64_t), st);
       if (err != hipSuccess) return hip_fail(err, "clock probe reset");
       a.clk = p->clk;
@@ -515,6 +518,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
       p->clk_written = true;
     }
     hipError_t err = p->dtype == PGSR_F32    ? launch_attn_f32(a, st)
+                     : wide                  ? launch_attn_bf16_wide(a, st)
                      : pipe                  ? launch_attn_bf16_pipe(a, st)
                      : p->dtype == PGSR_BF16 ? launch_attn_bf16(a, st)
                                              : launch_attn_fp8(a, st);
@@ -737,7 +741,7 @@ int pgsr_pool_enable_timing(pgsr_pool* p, int on) {
 
 int pgsr_pool_set_prefill_kernel(pgsr_pool* p, int kind) {
   if (!p) return fail(PGSR_EINVAL, "pool is null");
-  if (kind != PGSR_PREFILL_AUTO && kind != PGSR_PREFILL_FOUR_WAVE)
+  if (kind != PGSR_PREFILL_AUTO && kind != PGSR_PREFILL_FOUR_WAVE && kind != PGSR_PREFILL_PIPELINED)
     return fail(PGSR_EINVAL, "unknown prefill kernel %d", kind);
   p->prefill_kind = kind;
   return ok();

@@ -124,8 +124,9 @@ class KVPool:
         N.check(N.lib.pgsr_pool_set_kv_scales(self._h, ks, vs))
 
     def set_prefill_kernel(self, kind: str) -> None:
-        """bf16 prefill kernel: "auto" (pipelined where it applies) or "four_wave"."""
-        code = {"auto": 0, "four_wave": 1}[kind]
+        """bf16 prefill kernel: "auto" (wide, else pipelined, where they apply),
+        "pipelined" (never the wide kernel) or "four_wave"."""
+        code = {"auto": 0, "four_wave": 1, "pipelined": 2}[kind]
         N.check(N.lib.pgsr_pool_set_prefill_kernel(self._h, code))
 
     # ---- kernel timing (HIP events recorded by the library on the call's stream) ----

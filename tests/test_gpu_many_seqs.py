@@ -20,21 +20,23 @@ def _blocks(n, B=16):
 
 
 CASES = [
-    # name, geometry, dtype, sequences, prefix range, query-length range
+    # name, geometry, dtype, sequences, prefix range, query-length range, bf16 kernel choice
     # decode: every query length <= 32 / G, pool with a workspace -> decode
     # kernel with key splits, 64 + 16 sequences in two launches
-    ("decode", W.AttnGeometry(4, 1, 64), "bf16", 80, (700, 1400), (1, 8)),
-    # pipelined bf16 prefill with split keys (few tiles per launch), 64 + 6
-    ("prefill_pipe", W.AttnGeometry(8, 2, 128), "bf16", 70, (300, 900), (1, 60)),
+    ("decode", W.AttnGeometry(4, 1, 64), "bf16", 80, (700, 1400), (1, 8), "auto"),
+    # wide bf16 prefill (16-token blocks) with split keys (few tiles per launch), 64 + 6
+    ("prefill_wide", W.AttnGeometry(8, 2, 128), "bf16", 70, (300, 900), (1, 60), "auto"),
+    # the two-wave pipelined kernel on the same shapes
+    ("prefill_pipe", W.AttnGeometry(8, 2, 128), "bf16", 70, (300, 900), (1, 60), "pipelined"),
     # four-wave bf16 kernel (head_dim 64), 64 + 66 + 2 sequences in three launches
-    ("prefill_four_wave", W.AttnGeometry(8, 2, 64), "bf16", 130, (100, 500), (1, 40)),
+    ("prefill_four_wave", W.AttnGeometry(8, 2, 64), "bf16", 130, (100, 500), (1, 40), "auto"),
     # fp32 kernel with split keys, 64 + 2
-    ("prefill_f32", W.AttnGeometry(4, 2, 64), "f32", 66, (100, 400), (1, 40)),
+    ("prefill_f32", W.AttnGeometry(4, 2, 64), "f32", 66, (100, 400), (1, 40), "auto"),
 ]
 
 
-@pytest.mark.parametrize("name,geom,dtype,n,p_rng,s_rng", CASES, ids=[c[0] for c in CASES])
-def test_many_sequences_split_and_decode_match_oracle(name, geom, dtype, n, p_rng, s_rng):
+@pytest.mark.parametrize("name,geom,dtype,n,p_rng,s_rng,kernel", CASES, ids=[c[0] for c in CASES])
+def test_many_sequences_split_and_decode_match_oracle(name, geom, dtype, n, p_rng, s_rng, kernel):
     log(f"many sequences: {name}, {n} sequences")
     rng = np.random.default_rng(len(name) * 100 + n)
     P = rng.integers(p_rng[0], p_rng[1] + 1, size=n).tolist()
@@ -47,6 +49,8 @@ def test_many_sequences_split_and_decode_match_oracle(name, geom, dtype, n, p_rn
     outs = []
     for split_q in (sum(S), 0):                    # with and without a workspace
         pool = make_pool(geom, dtype, nb, n, mbps, split_q=split_q, max_splits=32)
+        if dtype == "bf16":
+            pool.set_prefill_kernel(kernel)
         seqs = list(range(n))
         pq = torch.cat([dev(e.q[:e.prefix], dtype) for e in eps])
         pk = torch.cat([dev(e.k[:e.prefix], dtype) for e in eps])

@@ -1,8 +1,9 @@
-"""The software-pipelined bf16 prefill kernel (head_dim 128, GQA groups
-dividing 32) against the four-wave kernel and the fp64 oracle.  Both kernels
-take every query row through the same sequence of operations, so their outputs
-must agree bit for bit; each must also meet the bf16 tolerance against the
-oracle.  Cases cover every group size the pipelined kernel takes, block sizes
+"""The bf16 prefill kernels for head_dim 128 and GQA groups dividing 32 (the
+wide kernel: one wave per SIMD, 64 rows per wave, 16-token blocks; the
+software-pipelined kernel: two waves per SIMD) against the four-wave kernel and
+the fp64 oracle.  All kernels take every query row through the same sequence
+of operations, so their outputs must agree bit for bit; each must also meet
+the bf16 tolerance against the oracle.  Cases cover every group size the pipelined kernel takes, block sizes
 16 / 32 / 64, crops not aligned to a block with NaN-poisoned tail slots,
 suffixes shorter than one query tile, tiles that straddle the diagonal, and
 several sequences of different lengths in one call; then the default kernel
@@ -64,10 +65,12 @@ def test_pipelined_equals_four_wave_and_oracle(hq, hkv, B, ps):
     rng = np.random.default_rng(hq * 7919 + B + sum(p for p, _ in ps))
     eps = [W.draw_episode(rng, geom, "bf16", P, S, P + S + 3) for P, S in ps]
     scale = 128 ** -0.5
-    pipe = _run("auto", geom, eps, B, scale)
+    auto = _run("auto", geom, eps, B, scale)          # the wide kernel where B = 16
+    pipe = _run("pipelined", geom, eps, B, scale)
     four = _run("four_wave", geom, eps, B, scale)
-    for e, a, b in zip(eps, pipe, four):
-        assert torch.equal(a, b), f"pipelined and four-wave kernels differ (P={e.prefix}, S={e.suffix})"
+    for e, a, p, f in zip(eps, auto, pipe, four):
+        assert torch.equal(p, f), f"pipelined and four-wave kernels differ (P={e.prefix}, S={e.suffix})"
+        assert torch.equal(a, f), f"default and four-wave kernels differ (P={e.prefix}, S={e.suffix})"
         assert_close(a.float().cpu().numpy(), oracle_suffix(e, scale), "bf16", f"P={e.prefix} S={e.suffix}")
 
 
