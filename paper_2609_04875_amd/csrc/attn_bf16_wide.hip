@@ -136,24 +136,17 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   // tiles [kt0, nu) hold only keys at or before every query of the workgroup
   const int nu = min(max((first_q + 1) / KT, kt0), n_kt);
 
-  // Q^T operands in AGPRs: lane holds Q[row][16*ds + 8*hh .. +7].
-  bf16x8 qf[QB][NDS];
+  // Q rows (lane: Q[row][16*ds + 8*hh .. +7]), requested first; they are
+  // scaled and moved to AGPRs after the first tile requests are issued, so
+  // the latencies of both overlap.
+  u32x4 qraw[QB][NDS];
+  bf16x8 qf[QB][NDS];                             // Q^T operands, in AGPRs once filled below
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
     const uint16_t* qg = qg_ + ((int64_t)(e.q_off + tok[b]) * a.n_q_heads + hq) * D + 8 * hh;
 #pragma unroll
-    for (int ds = 0; ds < NDS; ++ds) {
-      u32x4 raw = valid[b] ? *(const u32x4*)(qg + 16 * ds) : u32x4{0, 0, 0, 0};
-      f32x8 qx = __builtin_convertvector(__builtin_bit_cast(bf16x8, raw), f32x8) * a.scale_log2;
-      const bf16x8 qv = __builtin_convertvector(qx, bf16x8);   // Q scaled by scale * log2(e), rounded once
-      asm("; Q operand to AGPRs" : "=a"(qf[b][ds]) : "0"(qv));
-    }
+    for (int ds = 0; ds < NDS; ++ds) qraw[b][ds] = valid[b] ? *(const u32x4*)(qg + 16 * ds) : u32x4{0, 0, 0, 0};
   }
-  asm volatile("s_nop 3"
-               : "+a"(qf[0][0]), "+a"(qf[0][1]), "+a"(qf[0][2]), "+a"(qf[0][3]), "+a"(qf[0][4]),
-                 "+a"(qf[0][5]), "+a"(qf[0][6]), "+a"(qf[0][7]), "+a"(qf[1][0]), "+a"(qf[1][1]),
-                 "+a"(qf[1][2]), "+a"(qf[1][3]), "+a"(qf[1][4]), "+a"(qf[1][5]), "+a"(qf[1][6]),
-                 "+a"(qf[1][7]));
 
   const int32_t* __restrict__ row = tables + (int64_t)e.seq * a.max_bps;
   const int64_t head_base = (int64_t)a.layer * a.n_blocks * hkv + g;
@@ -376,6 +369,21 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
     request_all(buf_of(kt0 + 1), id1);
     request_all(buf_of(kt0 + 2), id2);
   }
+  // Q^T operands in AGPRs, Q scaled by scale * log2(e) and rounded once
+#pragma unroll
+  for (int b = 0; b < QB; ++b)
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds) {
+      asm volatile("" : "+v"(qraw[b][ds]));     // after the requests above
+      f32x8 qx = __builtin_convertvector(__builtin_bit_cast(bf16x8, qraw[b][ds]), f32x8) * a.scale_log2;
+      const bf16x8 qv = __builtin_convertvector(qx, bf16x8);
+      asm("; Q operand to AGPRs" : "=a"(qf[b][ds]) : "0"(qv));
+    }
+  asm volatile("s_nop 3"
+               : "+a"(qf[0][0]), "+a"(qf[0][1]), "+a"(qf[0][2]), "+a"(qf[0][3]), "+a"(qf[0][4]),
+                 "+a"(qf[0][5]), "+a"(qf[0][6]), "+a"(qf[0][7]), "+a"(qf[1][0]), "+a"(qf[1][1]),
+                 "+a"(qf[1][2]), "+a"(qf[1][3]), "+a"(qf[1][4]), "+a"(qf[1][5]), "+a"(qf[1][6]),
+                 "+a"(qf[1][7]));
   bar();
 
   f32x16 sa[QB][2], sb[QB][2];
