@@ -176,8 +176,11 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
     const int blk = j & 3;
     const char* src = (j < 4 ? kc_h : vc_h) + (uint32_t)id[blk];
     const uint32_t img = lds0 + 2u * (buf + (j < 4 ? 0 : 8192) + blk * 2048);
-    asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1"
-                 :: "v"(j < 4 ? kdma : vdma), "s"(src), "s"(img), "s"(wofs) : "memory", "m0");
+    // the add sets SCC (declared, so that no carry of the compiler's 64-bit
+    // address arithmetic is held across it), and a load that reads M0 needs
+    // one wait state after an SALU write of M0
+    asm volatile("s_add_u32 m0, %2, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :: "v"(j < 4 ? kdma : vdma), "s"(src), "s"(img), "s"(wofs) : "memory", "m0", "scc");
   };
   auto request_all = [&](int buf, const int (&id)[KB]) {
 #pragma unroll

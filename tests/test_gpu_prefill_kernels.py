@@ -55,6 +55,9 @@ CASES = [
     (32, 4, 32, [(1021, 3)]),           # G = 8, fewer queries than one 32-row block
     (64, 4, 16, [(700, 45)]),           # G = 16
     (32, 8, 16, [(517, 90), (0, 33), (2000, 257), (63, 1)]),   # ragged batch in one call
+    # more query tiles per KV head than one XCD holds at once (the tiles of a
+    # head run in several rounds on its XCD)
+    (32, 8, 16, [(5, 2122), (0, 4160)]),
 ]
 
 
