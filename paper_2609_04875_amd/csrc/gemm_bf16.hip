@@ -185,6 +185,7 @@ void launch_tiles(int m, int n, int k, const void* x, const void* w, const void*
 
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s) {
+  if (gemm_bf16_wide_eligible(m, n, k)) return launch_gemm_bf16_wide(m, n, k, x, w, r, y, s);
   // 256 x 256 tiles when they give every CU at least one (256 CUs), else 128 x 128
   const int64_t big = (int64_t)((m + 255) / 256) * ((n + 255) / 256);
   if (big >= 256)

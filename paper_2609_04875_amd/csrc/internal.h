@@ -256,5 +256,10 @@ int replay_prefill_ws(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seq
 
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s);
+// One wave per SIMD, global->LDS tiles (products with at least 256 tiles of
+// 256 x 256, K a multiple of 32, m*k and n*k below 2^31); same bits as above.
+bool gemm_bf16_wide_eligible(int m, int n, int k);
+hipError_t launch_gemm_bf16_wide(int m, int n, int k, const void* x, const void* w, const void* r,
+                                 void* y, hipStream_t s);
 
 }  // namespace pgsr

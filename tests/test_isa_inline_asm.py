@@ -1,11 +1,13 @@
-"""Machine-code checks of the inline assembly in the wide prefill kernel
-(host only: the kernel is compiled to gfx950 assembly, nothing runs).
+"""Machine-code checks of the inline assembly in the kernels that issue
+global->LDS loads (the wide prefill kernel and the wide GEMM; host only: the
+kernels are compiled to gfx950 assembly, nothing runs).
 
-Its K/V tile requests are inline assembly that writes M0 with an SALU add and
-then issues a global->LDS load.  Two properties keep them correct:
+Their tile requests are inline assembly that writes M0 with an SALU
+instruction and then issues a global->LDS load.  Two properties keep them
+correct:
 
-* the add sets SCC, so no SCC value of compiler code may be live across a
-  request: an SCC consumer (s_addc_u32 finishing a 64-bit address, a
+* an SALU add into M0 sets SCC, so no SCC value of compiler code may be
+  live across such a request: an SCC consumer (s_addc_u32 finishing a 64-bit address, a
   conditional select or branch) after a request must see SCC written again by
   compiler code first (without that, a carry was lost and the high half of a
   cache-block address came out 4 GiB low);
@@ -29,20 +31,25 @@ SCC_WRITE = re.compile(
     r"|s_lshl\d_add_u32|s_(and|or)_saveexec_b64)\b")
 
 
-@pytest.fixture(scope="module")
-def wide_asm(tmp_path_factory):
+KERNELS = {"attn": ("attn_bf16_wide.hip", "attn_bf16_wide_kernel", 24),
+           "gemm": ("gemm_bf16_wide.hip", "gemm_bf16_wide_kernel", 32)}
+
+
+@pytest.fixture(scope="module", params=sorted(KERNELS))
+def wide_asm(request, tmp_path_factory):
     if not shutil.which(HIPCC) and not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
-    out = tmp_path_factory.mktemp("isa") / "wide.s"
+    src, kernel, min_requests = KERNELS[request.param]
+    out = tmp_path_factory.mktemp("isa") / (request.param + ".s")
     cmd = [HIPCC, "-O3", "-std=c++17", "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
            "-packed-fp32-ops", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}", "-x", "hip",
-           "--cuda-device-only", "-S", os.path.join(CSRC, "attn_bf16_wide.hip"), "-o", str(out)]
+           "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", str(out)]
     subprocess.run(cmd, check=True, capture_output=True)
     lines = [ln.split(";")[0].strip() if not ln.strip().startswith(";;#ASM") else ln.strip()
              for ln in out.read_text().splitlines()]
-    start = next(i for i, ln in enumerate(lines) if re.match(r"^_Z\w*attn_bf16_wide_kernel\w*:", ln))
+    start = next(i for i, ln in enumerate(lines) if re.match(rf"^_Z\w*{kernel}\w*:", ln))
     end = next(i for i in range(start, len(lines)) if lines[i].startswith("s_endpgm"))
-    return lines[start:end + 1]
+    return lines[start:end + 1], min_requests
 
 
 def _asm_blocks(lines):
@@ -57,11 +64,13 @@ def _asm_blocks(lines):
 
 
 def test_requests_present(wide_asm):
-    n = sum(1 for ln in wide_asm if ln.startswith("global_load_lds_dwordx4"))
-    assert n >= 24, f"expected the prologue's and the loop's tile requests, found {n}"
+    lines, min_requests = wide_asm
+    n = sum(1 for ln in lines if ln.startswith("global_load_lds_dwordx4"))
+    assert n >= min_requests, f"expected the prologue's and the loop's tile requests, found {n}"
 
 
 def test_no_compiler_scc_value_across_a_request(wide_asm):
+    wide_asm, _ = wide_asm
     bad = []
     for a, b in _asm_blocks(wide_asm):
         if not any(SCC_WRITE.match(ln) for ln in wide_asm[a + 1:b]):
@@ -79,6 +88,7 @@ def test_no_compiler_scc_value_across_a_request(wide_asm):
 
 
 def test_wait_state_between_m0_write_and_lds_load(wide_asm):
+    wide_asm, _ = wide_asm
     bad = []
     for a, b in _asm_blocks(wide_asm):
         body = [ln for ln in wide_asm[a + 1:b] if ln]
