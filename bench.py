@@ -654,7 +654,8 @@ def main() -> int:
     # which bf16 prefill kernel the library runs (the host's selection rule)
     fast = (w.dtype == "bf16" and g.head_dim == 128 and 32 % (g.n_q_heads // g.n_kv_heads) == 0)
     wide = (fast and args.prefill_kernel == "auto" and w.block_size == 16
-            and pool.n_blocks * g.n_kv_heads * 4096 <= 1 << 32)
+            and pool.n_blocks * g.n_kv_heads * 4096 <= 1 << 32
+            and max(p + s for p, s in zip(st.P, st.S)) <= 130816)
     pipe = fast and not wide and args.prefill_kernel in ("auto", "pipelined")
     single_call = st.calls_per_step == 1
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]

@@ -282,7 +282,8 @@ int pgsr_pool_last_clock(pgsr_pool *pool, void *stream, double *ghz, int64_t *cy
  * prefill form).  PGSR_PREFILL_AUTO (the default) runs, for a bf16 pool with
  * head_dim 128 and a GQA group dividing 32, the wide kernel (one wave per
  * SIMD, 64 query rows per wave, global->LDS tile loads) when the pool has
- * 16-token blocks and n_blocks * n_kv_heads * 4 KB <= 4 GB, else the
+ * 16-token blocks, n_blocks * n_kv_heads * 4 KB <= 4 GB and no sequence of
+ * the call reaches more than 130816 keys (prefix + suffix), else the
  * software-pipelined kernel (two waves per SIMD, 32 query rows per wave);
  * every other call runs the four-wave kernel.  PGSR_PREFILL_PIPELINED skips
  * the wide kernel; PGSR_PREFILL_FOUR_WAVE runs the four-wave kernel for every

@@ -40,9 +40,10 @@
 // of tile x - 1, so a request has two steps to land.  The requests are inline
 // assembly too; the loop issues no other vector memory operation, so "all but
 // the latest 8 requests complete" (s_waitcnt vmcnt(8)) before the one barrier
-// of a step proves the tiles the next step reads are in LDS.  Block ids are
-// scalar loads issued after a step's last LDS operand read (a scalar load in
-// flight would turn every LDS wait into a full wait).
+// of a step proves the tiles the next step reads are in LDS.  Block ids come
+// from a copy of the workgroup's part of the block table in LDS (one 16-byte
+// read per tile, in order with the operand reads); the loop issues no scalar
+// load (one in flight would turn every LDS wait into a full wait).
 //
 // Step schedule.  Tiles whose keys all precede the workgroup's first query
 // need no mask.  Step t is 64 issue slots fenced by sched_barrier, one product
@@ -75,6 +76,7 @@ constexpr int kWQB = 2;             // 32-row query blocks per wave
 constexpr int kWKT = 64;            // keys per tile
 constexpr int kWBufElems = 16384;   // elements per LDS tile buffer (K 8192, V^T 8192)
 constexpr float kWSlack = 8.f;      // lazy rescale threshold, log2 units
+constexpr int kWMaxIdt = 8192;      // block-table entries a workgroup keeps in LDS
 
 // f(integral_constant<int, I>) for I = 0, 1, ... in order, at compile time.
 template <class F, int... I>
@@ -93,6 +95,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   constexpr int NKS = KT / 16;             // 16-key steps of PV
   static_assert(KB == 4 && NW == 4 && QB == 2 && NDS == 8 && NDB == 4 && NKS == 4, "slot layout");
   __shared__ __attribute__((aligned(16))) uint16_t lds[4 * kWBufElems];
+  __shared__ __attribute__((aligned(16))) uint32_t idt[kWMaxIdt];
 
   uint64_t clk0 = 0, rt0 = 0;
   if (a.clk) {
@@ -156,10 +159,24 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   // 32-bit range: the launcher takes only pools with n_blocks * n_kv_heads *
   // 4 KB < 4 GB); ids past the sequence's last block are clamped to it.
   const uint32_t blk_bytes = (uint32_t)hkv * (B * D * 2);
-  auto tile_ids = [&](int kt, int (&id)[KB]) {
+  auto tile_ids_s = [&](int kt, int (&id)[KB]) {
 #pragma unroll
     for (int j = 0; j < KB; ++j) id[j] = (int)((uint32_t)row[min(kt * KB + j, last_blk)] * blk_bytes);
   };
+  // The workgroup's block offsets (blocks kt0 * KB .. last_blk) in LDS, so
+  // that the loop takes its block ids with LDS reads (in order with the
+  // operand reads) instead of scalar loads (a scalar load in flight turns
+  // every LDS wait into a full wait).  Filled before the first barrier.
+  // Entries past last_blk repeat it (tiles up to n_kt + 3 are requested).
+  const int blk0 = kt0 * KB;
+  for (int i = tid; i < (n_kt + 4 - kt0) * KB; i += NW * 64)
+    idt[i] = (uint32_t)row[min(blk0 + i, last_blk)] * blk_bytes;
+  auto ids_fetch = [&](int kt) { return *(const u32x4*)&idt[(kt - kt0) * KB]; };
+  auto ids_use = [&](const u32x4& v, int (&id)[KB]) {
+#pragma unroll
+    for (int j = 0; j < KB; ++j) id[j] = __builtin_amdgcn_readfirstlane((int)v[j]);
+  };
+  auto tile_ids = [&](int kt, int (&id)[KB]) { ids_use(ids_fetch(kt), id); };
   const char* kc_h = (const char*)(kc + head_base * (B * D));
   const char* vc_h = (const char*)(vc + head_base * (B * D));
   const uint32_t wofs = (uint32_t)w * 1024;         // byte offset of wave w's run in an image
@@ -364,10 +381,10 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   int idn[KB];
   {
     int id0[KB], id1[KB], id2[KB];
-    tile_ids(kt0, id0);
-    tile_ids(kt0 + 1, id1);
-    tile_ids(kt0 + 2, id2);
-    tile_ids(kt0 + 3, idn);
+    tile_ids_s(kt0, id0);
+    tile_ids_s(kt0 + 1, id1);
+    tile_ids_s(kt0 + 2, id2);
+    tile_ids_s(kt0 + 3, idn);
     request_all(buf_of(kt0), id0);
     request_all(buf_of(kt0 + 1), id1);
     request_all(buf_of(kt0 + 2), id2);
@@ -411,6 +428,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       mxa[b] = -INFINITY;
     }
     bf16x8 opnd[32];                            // 16 K then 16 V^T operands
+    u32x4 idv;                                  // block offsets of tile t + 4
     f32x2 ex[4];                                // exponentials awaiting their rounding
     auto read_op = [&](int u) {
       opnd[u] = u < 16 ? k_op(tk, u % 2, u / 2) : v_op(tv, (u - 16) / 4, (u - 16) % 4);
@@ -432,6 +450,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
         mfma_o(opnd[i / 2], __builtin_bit_cast(bf16x8, pw[b][ks]), oacc[b][db]);
       }
       if constexpr (i == 33) s_sync(sn);
+      if constexpr (i == 40) idv = ids_fetch(t + 4);
       // keep the operand of slots i-3 and i-2 allocated until here, so that
       // no VALU result lands in registers a product may still be reading
       if constexpr (i >= 3 && (i - 3) % 2 == 0) asm volatile("" ::"v"(opnd[(i - 3) / 2]));
@@ -467,7 +486,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       __builtin_amdgcn_sched_barrier(0);
     };
     static_for(slot, std::make_integer_sequence<int, 64>{});
-    tile_ids(t + 4, idn);
+    ids_use(idv, idn);
     // row-sum terms of P(t) in the fixed order (per row block: ks, then the
     // 4 pairs alternating between two partial sums)
 #pragma unroll
@@ -600,7 +619,10 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
 
 }  // namespace
 
-bool attn_bf16_wide_eligible(int head_dim, int group, int block_size, int64_t n_blocks, int n_kv_heads) {
+bool attn_bf16_wide_eligible(int head_dim, int group, int block_size, int64_t n_blocks, int n_kv_heads,
+                             int64_t max_kv_len) {
+  // a workgroup's LDS block table holds (key tiles + 4) * 4 entries
+  if ((max_kv_len + kWKT - 1) / kWKT + 4 > kWMaxIdt / 4) return false;
   return head_dim == 128 && block_size == 16 && group >= 1 && group <= 32 && 32 % group == 0 &&
          n_blocks * n_kv_heads * 4096 <= ((int64_t)1 << 32);
 }
@@ -608,7 +630,9 @@ bool attn_bf16_wide_eligible(int head_dim, int group, int block_size, int64_t n_
 hipError_t launch_attn_bf16_wide(const AttnArgs& a, hipStream_t s) {
   if (a.n <= 0 || a.n_tiles <= 0) return hipSuccess;
   const int group = a.n_q_heads / a.n_kv_heads;
-  if (!attn_bf16_wide_eligible(a.head_dim, group, a.block_size, a.n_blocks, a.n_kv_heads))
+  int64_t max_kv = 0;
+  for (int i = 0; i < a.n; ++i) max_kv = max(max_kv, (int64_t)a.e[i].prefix + a.e[i].q_len);
+  if (!attn_bf16_wide_eligible(a.head_dim, group, a.block_size, a.n_blocks, a.n_kv_heads, max_kv))
     return hipErrorInvalidValue;
   const dim3 grid(a.n_tiles * a.n_kv_heads * a.n_splits), blk(kWW * 64);
   hipLaunchKernelGGL(attn_bf16_wide_kernel, grid, blk, 0, s, a, a.tables, (const uint16_t*)a.q,

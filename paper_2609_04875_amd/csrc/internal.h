@@ -218,8 +218,11 @@ int attn_bf16_pipe_tile_tokens(int group);
 hipError_t launch_attn_bf16_pipe(const AttnArgs& a, hipStream_t s);
 // The same tiles and bits with one wave per SIMD holding 64 query rows and
 // global->LDS tile loads: 16-token blocks, pools whose layer-head block range
-// fits 32-bit byte offsets.  Tile tokens as attn_bf16_pipe_tile_tokens.
-bool attn_bf16_wide_eligible(int head_dim, int group, int block_size, int64_t n_blocks, int n_kv_heads);
+// fits 32-bit byte offsets, sequences of up to 130816 keys (a workgroup's
+// part of the block table sits in LDS).  Tile tokens as
+// attn_bf16_pipe_tile_tokens.
+bool attn_bf16_wide_eligible(int head_dim, int group, int block_size, int64_t n_blocks, int n_kv_heads,
+                             int64_t max_kv_len);
 hipError_t launch_attn_bf16_wide(const AttnArgs& a, hipStream_t s);
 // Same kernel over an FP8 E4M3 cache: codes widen to bf16 exactly on the way
 // into LDS; the K scale is in scale_log2, the V scale in o_scale.
@@ -257,7 +260,7 @@ int replay_prefill_ws(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seq
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s);
 // One wave per SIMD, global->LDS tiles (products with at least 256 tiles of
-// 256 x 256, K a multiple of 32, m*k and n*k below 2^31); same bits as above.
+// 256 x 256, K a multiple of 64, m*k and n*k below 2^31); same bits as above.
 bool gemm_bf16_wide_eligible(int m, int n, int k);
 hipError_t launch_gemm_bf16_wide(int m, int n, int k, const void* x, const void* w, const void* r,
                                  void* y, hipStream_t s);

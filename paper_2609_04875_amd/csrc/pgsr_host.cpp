@@ -419,8 +419,10 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
   // pool has a workspace (so batching already decides the rounding order).
   bool decode = p->dtype != PGSR_F32 && ws_bytes > 0;
   for (const Seg& g : segs) decode = decode && g.q_len <= 32 / group;
+  int64_t max_kv = 0;
+  for (const Seg& g : segs) max_kv = std::max<int64_t>(max_kv, (int64_t)g.prefix + g.q_len);
   const bool wide = p->dtype == PGSR_BF16 && p->prefill_kind == PGSR_PREFILL_AUTO &&
-                    attn_bf16_wide_eligible(p->d, group, p->B, p->n_blocks, p->hkv);
+                    attn_bf16_wide_eligible(p->d, group, p->B, p->n_blocks, p->hkv, max_kv);
   const bool pipe = !wide && p->dtype == PGSR_BF16 &&
                     (p->prefill_kind == PGSR_PREFILL_AUTO || p->prefill_kind == PGSR_PREFILL_PIPELINED) &&
                     attn_bf16_pipe_eligible(p->d, group);
