@@ -1,31 +1,35 @@
 // Dense bf16 projection Y = X W^T (+ R), large-product path: one wave per
 // SIMD, each owning a 128 x 128 block of a 256 x 256 output tile, the 256
 // accumulators in AGPRs, X and W tiles brought to LDS by global->LDS loads,
-// and every K step laid out as 32 fenced issue slots.
+// and every K step laid out as 64 fenced issue slots.
 //
-// K advances 32 at a time.  A step needs a 256 x 32 tile of X and one of W
-// (16 KB each, one 32 KB LDS buffer); four buffers rotate and step kt
-// requests step kt + 3 into the buffer step kt - 1 used.  A wave requests 4
-// runs of 1 KB of each image per step (16 rows x 64 bytes per run) with
-// global_load_lds_dwordx4: lane l's 16 bytes land at byte 16 l of the run, so
-// the image layout is chosen through the global chunk each lane fetches:
-// chunk c of row j sits at slot c ^ ((j / 4) mod 4), which spreads the 16
-// rows an operand read touches over all 64 banks.
+// K advances 64 at a time.  A step needs a 256 x 64 tile of X and one of W
+// (32 KB each, one 64 KB LDS buffer); two buffers alternate.  A wave
+// requests 8 runs of 1 KB of each image per step (8 rows x 128 bytes per
+// run, whole cache lines) with global_load_lds_dwordx4: lane l's 16 bytes
+// land at byte 16 l of the run, so the image layout is chosen through the
+// global chunk each lane fetches: chunk c of row j sits at slot
+// c ^ ((j / 2) mod 8), which spreads the 16 rows an operand read touches
+// over all 64 banks.
 //
 // Step schedule (slot s = one v_mfma_f32_32x32x16_bf16: k slice s / 16, W
-// sub-tile (s / 4) mod 4, X sub-tile s mod 4).  Slots 0-15 multiply slice 0
-// while the operands of slice 1 are read, one read every other slot; then
-// this wave's requests of step kt - 2 are waited for (s_waitcnt vmcnt(8):
-// only step kt - 1's are left) and the workgroup meets at a barrier, after
-// which step kt + 1's tiles are in LDS and step kt - 1's buffer is free;
-// slots 16-31 multiply slice 1 while this step's 8 requests go out and the
-// operands of slice 0 of step kt + 1 are read.  Every operand register is
-// rewritten at least six slots after the last product that read it.  The
-// loop issues no other vector memory operation, so the vmcnt count is exact.
+// sub-tile (s / 4) mod 4, X sub-tile s mod 4; each slice's 8 operands in a
+// register set of their own).  Slots 0-23 read slices 1-3 of this step, one
+// operand per slot.  At slot 24 the wave waits for its requests of step
+// kt + 1 (issued from slot 24 of the previous step on) and its LDS reads,
+// and the workgroup meets at the step's one barrier: step kt + 1's tiles are
+// then in LDS and every wave has read all of step kt's buffer.  Slots 24-39
+// read slice 0 of step kt + 1, and slots 24-54 issue this step's 16 requests
+// (step kt + 2, into the buffer just read), one every other slot, so that
+// the four waves' loads reach the CU's load path spread over the step.  The
+// loop is unrolled by two, so each buffer's operand addresses are
+// loop-invariant registers plus immediates.  The loop issues no other
+// vector memory operation, so the vmcnt count is exact.
 //
-// The products are inline assembly (AGPR accumulators), and the wait states
+// The products are inline assembly (AGPR accumulators); the 19 wait states
 // the compiler would insert before VALU reads of the accumulators are
-// written out at the end of every step (they overlap the last product).  The
+// written out after the loop, and the epilogue reads each m sub-tile's
+// accumulators only after an assembly statement ordered after them.  The
 // requests are inline assembly too: the compiler's builtin would make every
 // later LDS read wait for them.  Each request moves its LDS address into M0
 // and waits one state before the load reads M0.
@@ -54,11 +58,11 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kGB = 256;               // output tile edge (M and N)
-constexpr int kGK = 32;                // K step
-constexpr int kGNB = 4;                // LDS buffers
+constexpr int kGK = 64;                // K step
+constexpr int kGNB = 2;                // LDS buffers
 constexpr int kGImg = kGB * kGK;       // elements of one X or W image
 constexpr int kGBuf = 2 * kGImg;       // elements of one buffer (X image, then W image)
-constexpr int kGRuns = 4;              // 1 KB runs per wave and image per step
+constexpr int kGRuns = 8;              // 1 KB runs per wave and image per step
 constexpr int kGGroupM = 8;            // tile rows per group of the tile order
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
@@ -68,8 +72,8 @@ __device__ __forceinline__ void static_for(F&& f, std::integer_sequence<int, I..
   (f(std::integral_constant<int, I>{}), ...);
 }
 
-// swizzle of the 16-byte chunk slot within a 64-byte image row
-__device__ __forceinline__ int gsw(int row) { return (row >> 2) & 3; }
+// swizzle of the 16-byte chunk slot within a 128-byte image row
+__device__ __forceinline__ int gsw(int row) { return (row >> 1) & 7; }
 
 __global__ void __launch_bounds__(256, 1)
 gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
@@ -92,38 +96,38 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
   const int lane = tid & 63, r = lane & 31, hh = lane >> 5;
   const int wm = (w & 1) * 128, wn = (w >> 1) * 128;
 
-  // Requests: wave w takes runs w, w + 4, w + 8, w + 12 of each image; run q
-  // = rows 16 q .. 16 q + 15, lane l -> row 16 q + l / 4, slot l % 4, chunk
-  // (l % 4) ^ gsw(row).  Rows past M or N read row M-1 or N-1 (their outputs
+  // Requests: wave w takes runs w, w + 4, ..., w + 28 of each image; run q =
+  // rows 8 q .. 8 q + 7, lane l -> row 8 q + l / 8, slot l % 8, chunk
+  // (l % 8) ^ gsw(row).  Rows past M or N read row M-1 or N-1 (their outputs
   // are never stored).  Byte offsets from the matrix start (the launcher
   // takes only M*K and N*K below 2^31 elements).
   uint32_t xoff[kGRuns], woff[kGRuns];
 #pragma unroll
   for (int j = 0; j < kGRuns; ++j) {
-    const int row = 16 * (w + 4 * j) + lane / 4;
-    const int c = (lane & 3) ^ gsw(row);
+    const int row = 8 * (w + 4 * j) + lane / 8;
+    const int c = (lane & 7) ^ gsw(row);
     xoff[j] = 2u * ((uint32_t)min(m0 + row, M - 1) * (uint32_t)K + 8u * c);
     woff[j] = 2u * ((uint32_t)min(n0 + row, N - 1) * (uint32_t)K + 8u * c);
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)&lds[0] + 1024u * w;
   const int nk = K / kGK;
-  // request q (0..7) of step kt: X run q (q < 4) or W run q - 4, into buffer
+  // request q (0..15) of step kt: X run q (q < 8) or W run q - 8, into buffer
   // kt mod kGNB; steps past the last read the last step again (its buffer is
   // never read), so every step issues the same number of requests
   auto request = [&](int kt, int q) {
     const int ks = min(kt, nk - 1);
-    const char* src = (const char*)((q < 4 ? X : W) + (int64_t)ks * kGK);
-    const uint32_t img = lds0 + 2u * ((kt % kGNB) * kGBuf + (q < 4 ? 0 : kGImg)) + 4096u * (q & 3);
+    const char* src = (const char*)((q < 8 ? X : W) + (int64_t)ks * kGK);
+    const uint32_t img = lds0 + 2u * ((kt % kGNB) * kGBuf + (q < 8 ? 0 : kGImg)) + 4096u * (q & 7);
     asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-                 :: "v"(q < 4 ? xoff[q & 3] : woff[q & 3]), "s"(src), "s"(img) : "memory", "m0");
+                 :: "v"(q < 8 ? xoff[q & 7] : woff[q & 7]), "s"(src), "s"(img) : "memory", "m0");
   };
 
   // Operand reads: 32 x 16 slice ks of rows base + r at slot (2 ks + hh) ^
   // gsw(r) (every base is a multiple of 16).
-  int soff[2];
+  int soff[4];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) soff[ks] = r * kGK + (((2 * ks + hh) ^ gsw(r)) << 3);
-  bf16x8 wa[2][4], xb[2][4];
+  for (int ks = 0; ks < 4; ++ks) soff[ks] = r * kGK + (((2 * ks + hh) ^ gsw(r)) << 3);
+  bf16x8 wa[4][4], xb[4][4];
   // operand u (0..7) of slice ks from buffer buf: W sub-tile u / 2 for even u,
   // X sub-tile u / 2 for odd u
   auto read_op = [&](int buf, int ks, int u) {
@@ -140,38 +144,48 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
 
-  // prologue: steps 0..2 requested, step 0 landed, its slice-0 operands read
-  for (int kt = 0; kt < kGNB - 1; ++kt)
+  // prologue: steps 0 and 1 requested, step 0 landed, its slice-0 operands read
 #pragma unroll
-    for (int q = 0; q < 8; ++q) request(kt, q);
+  for (int q = 0; q < 16; ++q) request(0, q);
+#pragma unroll
+  for (int q = 0; q < 16; ++q) request(1, q);
   asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
 #pragma unroll
   for (int u = 0; u < 8; ++u) read_op(0, 0, u);
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt % kGNB, nxt = (kt + 1) % kGNB;
+  // step kt with its buffer parity CUR known at compile time, so that every
+  // operand address is a loop-invariant register plus an immediate
+  auto step = [&](auto cur_c, int kt) {
+    constexpr int cur = decltype(cur_c)::value, nxt = 1 - cur;
     auto slot = [&](auto ic) {
       constexpr int s = decltype(ic)::value;
       constexpr int ks = s / 16, i = (s / 4) % 4, j = s % 4;
-      if constexpr (s == 16) {
-        // step kt + 1 landed (all but this wave's latest 8 requests), and
-        // every wave is past step kt - 1
-        asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+      if constexpr (s == 24) {
+        // step kt + 1 landed (this wave's requests, issued from slot 24 of the
+        // previous step on, and the barrier for the other waves'), and every
+        // wave has read all of step kt's buffer, which the requests below
+        // refill with step kt + 2
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
       }
-      if constexpr (s % 2 == 0) {
-        if constexpr (ks == 0) read_op(cur, 1, s / 2);
-        else read_op(nxt, 0, (s - 16) / 2);
-      }
-      if constexpr (s >= 16 && s < 24) request(kt + kGNB - 1, s - 16);
+      // slices 1-3 of this step in slots 0-23, slice 0 of the next in 24-39
+      if constexpr (s < 24) read_op(cur, 1 + s / 8, s % 8);
+      else if constexpr (s < 40 && s % 2 == 0) read_op(nxt, 0, (s - 24) / 2);
+      // this step's requests, one every other slot
+      if constexpr (s >= 24 && s < 56 && s % 2 == 0) request(kt + 2, (s - 24) / 2);
       asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[i][j]) : "v"(wa[ks][i]), "v"(xb[ks][j]));
       __builtin_amdgcn_sched_barrier(0);
     };
-    static_for(slot, std::make_integer_sequence<int, 32>{});
-    // 19 wait states before any VALU read of the accumulators (they run in
-    // the shadow of the last product; at the loop's end they precede the
-    // epilogue's reads)
-    asm volatile("s_nop 15\n\ts_nop 3" ::: "memory");
+    static_for(slot, std::make_integer_sequence<int, 64>{});
+  };
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(std::integral_constant<int, 0>{}, kt);
+    step(std::integral_constant<int, 1>{}, kt + 1);
   }
+  if (kt < nk) step(std::integral_constant<int, 0>{}, kt);
+  // 19 wait states before any VALU read of the accumulators (the epilogue
+  // reads each m sub-tile's after an assembly statement ordered after this)
+  asm volatile("s_nop 15\n\ts_nop 3" ::: "memory");
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // requests past the end, before LDS is handed on
 
   // acc[i][j] lane (r, hh), register q: n = wn + 32i + 8(q/4) + 4hh + q%4,

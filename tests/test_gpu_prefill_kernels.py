@@ -148,3 +148,23 @@ def test_pipelined_full_reset_equals_replay_at_8b_crop():
     ref = oracle_suffix(ep, scale, rows=rows)
     got = o.reshape(S * 32, 128)[torch.from_numpy(rows).cuda()]
     assert_close(got.float().cpu().numpy(), ref, "bf16", "8B crop, sampled rows")
+
+
+@pytest.mark.parametrize("P,S", [(130700, 100), (130900, 100)])
+def test_longest_sequences_for_the_lds_block_table(P, S):
+    """A sequence at the wide kernel's limit (130816 keys: a workgroup's copy
+    of the block table fills its LDS share) and one just past it (the host
+    then runs the pipelined kernel): the default kernel bitwise against the
+    four-wave one, and sampled rows against the oracle."""
+    geom = W.AttnGeometry(32, 8, 128)
+    log(f"longest sequences: P={P} S={S}")
+    rng = np.random.default_rng(P)
+    eps = [W.draw_episode(rng, geom, "bf16", P, S, P + S + 3)]
+    scale = 128 ** -0.5
+    auto = _run("auto", geom, eps, 16, scale)[0]
+    four = _run("four_wave", geom, eps, 16, scale)[0]
+    assert torch.equal(auto, four), f"default and four-wave kernels differ (P={P}, S={S})"
+    rows = np.arange(0, S * geom.n_q_heads, 97)
+    ref = oracle_suffix(eps[0], scale, rows=rows)
+    got = auto.reshape(-1, 128)[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    assert_close(got, ref, "bf16", f"P={P} S={S}")

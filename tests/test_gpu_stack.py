@@ -26,9 +26,10 @@ def _f64(t: torch.Tensor) -> np.ndarray:
                                        (300, 1024, 520, True), (257, 264, 1024, False),
                                        (1000, 1024, 8192, True), (4100, 4104, 200, True),
                                        # products with at least 256 tiles of 256 x 256 and K a
-                                       # multiple of 32 (one wave per SIMD, global->LDS tiles):
-                                       # ragged edges with a residual, and a single K step
-                                       (4100, 4104, 224, True), (4097, 4096, 32, False)])
+                                       # multiple of 64 (one wave per SIMD, global->LDS tiles):
+                                       # ragged edges with a residual, an odd number of K steps,
+                                       # and a single K step
+                                       (4100, 4104, 192, True), (4097, 4096, 64, False)])
 def test_gemm_matches_fp64(m, n, k, res):
     from paper_2609_04875_amd import gemm_bf16
     rng = np.random.default_rng(m * 7 + n)
