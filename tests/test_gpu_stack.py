@@ -76,12 +76,13 @@ def test_gemm_tile_shapes_agree_bitwise():
     assert torch.equal(part, full[1000:1300])
 
 
-def test_gemm_residual_may_alias_output():
+@pytest.mark.parametrize("m,n,k", [(64, 128, 256), (4096, 4096, 128)])   # both kernels
+def test_gemm_residual_may_alias_output(m, n, k):
     from paper_2609_04875_amd import gemm_bf16
     rng = np.random.default_rng(4)
-    x = _bf16_dev(rng.standard_normal((64, 256)))
-    w = _bf16_dev(rng.standard_normal((128, 256)) / 16)
-    r = _bf16_dev(rng.standard_normal((64, 128)))
+    x = _bf16_dev(rng.standard_normal((m, k)))
+    w = _bf16_dev(rng.standard_normal((n, k)) / 16)
+    r = _bf16_dev(rng.standard_normal((m, n)))
     want = gemm_bf16(x, w, r=r)
     gemm_bf16(x, w, r=r, out=r)
     assert torch.equal(r, want)
