@@ -44,6 +44,8 @@
 
 #include "internal.h"
 
+// The requests write M0 (the LDS address of a global->LDS load) from inline
+// assembly that lists it as clobbered; nothing else in this file uses M0.
 #pragma clang diagnostic ignored "-Winline-asm"
 
 namespace pgsr {
