@@ -1,22 +1,24 @@
 // Dense bf16 projection Y = X W^T (+ R) for the stacked-layer transition F,
 // with W in the linear-layer layout [n][k]: fp32 accumulation on
-// v_mfma_f32_32x32x16_bf16 and one round-to-nearest-even store.
+// v_mfma_f32_16x16x32_bf16 (k in slices of 32 from 0) and one
+// round-to-nearest-even store.  Products with at least 256 tiles of
+// 256 x 256 (and K a multiple of 64) run the one-wave-per-SIMD kernel of
+// gemm_bf16_wide.hip; this register-staged kernel takes every other product.
 //
 // A workgroup computes a BM x BN output tile with WGM x WGN waves, each wave a
-// (TM * 32) x (TN * 32) block as TM x TN MFMA tiles: 256 x 256 with 8 waves of
-// 2 x 4 tiles for large products (one workgroup per CU, 144 KB of LDS), and
-// 128 x 128 with 4 waves of 2 x 2 tiles when the large tile would leave CUs
-// idle.  K advances 64 at a time through padded, double-buffered LDS tiles of
-// X rows and W rows (both k-contiguous, so both MFMA operands are 16-byte
-// reads); the next K step is loaded into registers while the current one is
-// multiplied.  The product is formed transposed (A = W rows, B = X rows): a
-// lane then holds one output row and groups of 4 consecutive columns, stored
-// as 8-byte writes.  Output tiles are numbered so that each XCD (workgroup id
-// mod 8) takes a contiguous run of them, walked in groups of 8 tile rows, and
-// the workgroups sharing an XCD's L2 share their X and W panels.  The K loop
-// never splits and both tile shapes run the same products in the same order,
-// so each output element's accumulation order is fixed (rows of Y are
-// bitwise independent of which other rows share the launch).
+// (TM * 32) x (TN * 32) block as (2 TM) x (2 TN) 16 x 16 MFMA tiles: 128 x 128
+// with 4 waves of 64 x 64, two workgroups per CU.  K advances 64 at a time
+// through padded, double-buffered LDS tiles of X rows and W rows (both
+// k-contiguous, so both MFMA operands are 16-byte reads); the next K steps
+// are loaded into registers while the current one is multiplied.  The
+// product is formed transposed (A = W rows, B = X rows): a lane then holds
+// one output row and 4 consecutive columns per sub-tile, stored as 8-byte
+// writes.  Output tiles are numbered so that each XCD (workgroup id mod 8)
+// takes a contiguous run of them, walked in groups of 8 tile rows, and the
+// workgroups sharing an XCD's L2 share their X and W panels.  The K loop
+// never splits and both kernels run the same products in the same order, so
+// each output element's accumulation order is fixed (rows of Y are bitwise
+// independent of which other rows share the launch).
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -27,7 +29,6 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -60,7 +61,7 @@ gemm_bf16_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
   const int idx = t - grp * kGroupM * n_tn;
   const int m0 = (first_m + idx % gsize) * BM, n0 = (idx / gsize) * BN;
 
-  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, r = lane & 31, hh = lane >> 5;
+  const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63, r16 = lane & 15, g4 = lane >> 4;
   const int wm = (wv % WGM) * TM * 32, wn = (wv / WGM) * TN * 32;
 
   // Loads read clamped (always valid) addresses, so the load sequence has no
@@ -101,30 +102,33 @@ gemm_bf16_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
     }
   };
 
-  f32x16 acc[TN][TM];   // [n sub-tile][m sub-tile], element (n, m)
+  // 16 x 16 output sub-tiles: a wave's (TM * 32) x (TN * 32) block is
+  // (2 TM) x (2 TN) of them
+  f32x4 acc[2 * TN][2 * TM];   // [n sub-tile][m sub-tile], element (n, m)
 #pragma unroll
-  for (int i = 0; i < TN; ++i)
+  for (int i = 0; i < 2 * TN; ++i)
 #pragma unroll
-    for (int j = 0; j < TM; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < 2 * TM; ++j) acc[i][j] = f32x4{};
 
   const int nk = (K + BK - 1) / BK;
+  // operand = 16 rows x 32 k (k slice ks): lane -> row r16, k 32 ks + 8 g4 .. +7
   auto mma = [&](int buf) {
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 wa[TN], xb[TM];
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      bf16x8 wa[2 * TN], xb[2 * TM];
 #pragma unroll
-      for (int i = 0; i < TN; ++i)
+      for (int i = 0; i < 2 * TN; ++i)
         wa[i] = __builtin_bit_cast(
-            bf16x8, *(const u32x4*)&ws[buf][(wn + 32 * i + r) * LDK + ks * 16 + 8 * hh]);
+            bf16x8, *(const u32x4*)&ws[buf][(wn + 16 * i + r16) * LDK + ks * 32 + 8 * g4]);
 #pragma unroll
-      for (int j = 0; j < TM; ++j)
+      for (int j = 0; j < 2 * TM; ++j)
         xb[j] = __builtin_bit_cast(
-            bf16x8, *(const u32x4*)&xs[buf][(wm + 32 * j + r) * LDK + ks * 16 + 8 * hh]);
+            bf16x8, *(const u32x4*)&xs[buf][(wm + 16 * j + r16) * LDK + ks * 32 + 8 * g4]);
 #pragma unroll
-      for (int i = 0; i < TN; ++i)
+      for (int i = 0; i < 2 * TN; ++i)
 #pragma unroll
-        for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[i], xb[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 2 * TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[i], xb[j], acc[i][j], 0, 0, 0);
     }
   };
   // step kt: its chunks (register set kt % 2) go to LDS buffer kt % 2, last
@@ -144,30 +148,27 @@ gemm_bf16_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
     kstep(1, kt + 1);
   }
   if (kt < nk) kstep(0, kt);
-  // acc[i][j] lane (r, hh), register q: n = wn + 32i + 8(q/4) + 4hh + q%4,
-  // m = wm + 32j + r.
+  // acc[i][j] lane (r16, g4), register q: n = wn + 16i + 4g4 + q,
+  // m = wm + 16j + r16.
 #pragma unroll
-  for (int j = 0; j < TM; ++j) {
-    const int m = m0 + wm + 32 * j + r;
+  for (int j = 0; j < 2 * TM; ++j) {
+    const int m = m0 + wm + 16 * j + r16;
     if (m >= M) continue;
 #pragma unroll
-    for (int i = 0; i < TN; ++i)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int n = n0 + wn + 32 * i + 8 * q4 + 4 * hh;
-        if (n >= N) continue;                      // N is a multiple of 8: whole group in or out
-        const int64_t o = (int64_t)m * N + n;
-        f32x4 v = {acc[i][j][4 * q4 + 0], acc[i][j][4 * q4 + 1], acc[i][j][4 * q4 + 2],
-                   acc[i][j][4 * q4 + 3]};
-        if (R) {
-          const u32x2 rb = *(const u32x2*)(R + o);
-          v[0] += bf16_to_f32((uint16_t)(rb[0] & 0xFFFF));
-          v[1] += bf16_to_f32((uint16_t)(rb[0] >> 16));
-          v[2] += bf16_to_f32((uint16_t)(rb[1] & 0xFFFF));
-          v[3] += bf16_to_f32((uint16_t)(rb[1] >> 16));
-        }
-        *(bf16x4*)(Y + o) = __builtin_convertvector(v, bf16x4);
+    for (int i = 0; i < 2 * TN; ++i) {
+      const int n = n0 + wn + 16 * i + 4 * g4;
+      if (n >= N) continue;                        // N is a multiple of 8: whole group in or out
+      const int64_t o = (int64_t)m * N + n;
+      f32x4 v = acc[i][j];
+      if (R) {
+        const u32x2 rb = *(const u32x2*)(R + o);
+        v[0] += bf16_to_f32((uint16_t)(rb[0] & 0xFFFF));
+        v[1] += bf16_to_f32((uint16_t)(rb[0] >> 16));
+        v[2] += bf16_to_f32((uint16_t)(rb[1] & 0xFFFF));
+        v[3] += bf16_to_f32((uint16_t)(rb[1] >> 16));
       }
+      *(bf16x4*)(Y + o) = __builtin_convertvector(v, bf16x4);
+    }
   }
 }
 
@@ -186,12 +187,8 @@ void launch_tiles(int m, int n, int k, const void* x, const void* w, const void*
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s) {
   if (gemm_bf16_wide_eligible(m, n, k)) return launch_gemm_bf16_wide(m, n, k, x, w, r, y, s);
-  // 256 x 256 tiles when they give every CU at least one (256 CUs), else 128 x 128
-  const int64_t big = (int64_t)((m + 255) / 256) * ((n + 255) / 256);
-  if (big >= 256)
-    launch_tiles<4, 2, 2, 4, 1>(m, n, k, x, w, r, y, s);
-  else
-    launch_tiles<2, 2, 2, 2, 2>(m, n, k, x, w, r, y, s);
+  // every other product: 128 x 128 tiles, two workgroups per CU
+  launch_tiles<2, 2, 2, 2, 2>(m, n, k, x, w, r, y, s);
   return hipGetLastError();
 }
 

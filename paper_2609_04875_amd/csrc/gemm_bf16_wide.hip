@@ -124,60 +124,49 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
                  :: "v"(q < 8 ? xoff[q & 7] : woff[q & 7]), "s"(src), "s"(img) : "memory", "m0");
   };
 
-  // Operand reads: 32 x 16 slice ks of rows base + r at slot (2 ks + hh) ^
-  // gsw(r) (every base is a multiple of 16).
-  int soff[4];
+  // 16x16x32 products: operand = 16 rows x 32 k; lane l -> row l % 16, k
+  // group l / 16 (8 values), i.e. chunk 4 ks + l / 16 of the row
+  const int r16 = lane & 15, g4 = lane >> 4;
+  int soff[2];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) soff[ks] = r * kGK + (((2 * ks + hh) ^ gsw(r)) << 3);
-  bf16x8 wa[4][4], xb[4][4];
-  // operand u (0..7) of slice ks from buffer buf: W sub-tile u / 2 for even u,
-  // X sub-tile u / 2 for odd u
+  for (int ks = 0; ks < 2; ++ks) soff[ks] = r16 * kGK + (((4 * ks + g4) ^ gsw(r16)) << 3);
+  bf16x8 wa[2][8], xb[2][8];
+  // operand u (0..15) of slice ks: W sub-tile u / 2 (even u), X sub-tile u / 2 (odd u)
   auto read_op = [&](int buf, int ks, int u) {
     const uint16_t* img = &lds[buf * kGBuf + ((u & 1) ? 0 : kGImg)];
-    const int base = ((u & 1) ? wm : wn) + 32 * (u >> 1);
+    const int base = ((u & 1) ? wm : wn) + 16 * (u >> 1);
     const bf16x8 v = __builtin_bit_cast(bf16x8, *(const u32x4*)&img[base * kGK + soff[ks]]);
     if (u & 1) xb[ks][u >> 1] = v;
     else wa[ks][u >> 1] = v;
   };
 
-  f32x16 acc[4][4];     // [n sub-tile][m sub-tile], element (n, m)
+  f32x4 acc[8][8];      // [n sub-tile][m sub-tile]
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{};
 
-  // prologue: steps 0 and 1 requested, step 0 landed, its slice-0 operands read
 #pragma unroll
   for (int q = 0; q < 16; ++q) request(0, q);
 #pragma unroll
   for (int q = 0; q < 16; ++q) request(1, q);
   asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
 #pragma unroll
-  for (int u = 0; u < 8; ++u) read_op(0, 0, u);
+  for (int u = 0; u < 16; ++u) read_op(0, 0, u);
 
-  // step kt with its buffer parity CUR known at compile time, so that every
-  // operand address is a loop-invariant register plus an immediate
   auto step = [&](auto cur_c, int kt) {
     constexpr int cur = decltype(cur_c)::value, nxt = 1 - cur;
     auto slot = [&](auto ic) {
       constexpr int s = decltype(ic)::value;
-      constexpr int ks = s / 16, i = (s / 4) % 4, j = s % 4;
-      if constexpr (s == 24) {
-        // step kt + 1 landed (this wave's requests, issued from slot 24 of the
-        // previous step on, and the barrier for the other waves'), and every
-        // wave has read all of step kt's buffer, which the requests below
-        // refill with step kt + 2
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      }
-      // slices 1-3 of this step in slots 0-23, slice 0 of the next in 24-39
-      if constexpr (s < 24) read_op(cur, 1 + s / 8, s % 8);
-      else if constexpr (s < 40 && s % 2 == 0) read_op(nxt, 0, (s - 24) / 2);
-      // this step's requests, one every other slot
-      if constexpr (s >= 24 && s < 56 && s % 2 == 0) request(kt + 2, (s - 24) / 2);
-      asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc[i][j]) : "v"(wa[ks][i]), "v"(xb[ks][j]));
+      constexpr int ks = s / 64, i = (s / 8) % 8, j = s % 8;
+      if constexpr (s == 40) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if constexpr (s < 32 && s % 2 == 0) read_op(cur, 1, s / 2);
+      else if constexpr (s >= 64 && s < 96 && s % 2 == 0) read_op(nxt, 0, (s - 64) / 2);
+      if constexpr (s >= 40 && s < 104 && s % 4 == 0) request(kt + 2, (s - 40) / 4);
+      asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc[i][j]) : "v"(wa[ks][i]), "v"(xb[ks][j]));
       __builtin_amdgcn_sched_barrier(0);
     };
-    static_for(slot, std::make_integer_sequence<int, 64>{});
+    static_for(slot, std::make_integer_sequence<int, 128>{});
   };
   int kt = 0;
   for (; kt + 1 < nk; kt += 2) {
@@ -185,38 +174,31 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
     step(std::integral_constant<int, 1>{}, kt + 1);
   }
   if (kt < nk) step(std::integral_constant<int, 0>{}, kt);
-  // 19 wait states before any VALU read of the accumulators (the epilogue
-  // reads each m sub-tile's after an assembly statement ordered after this)
   asm volatile("s_nop 15\n\ts_nop 3" ::: "memory");
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // requests past the end, before LDS is handed on
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-  // acc[i][j] lane (r, hh), register q: n = wn + 32i + 8(q/4) + 4hh + q%4,
-  // m = wm + 32j + r.
+  // acc[i][j] lane l, register q: n = wn + 16 i + 4 (l / 16) + q, m = wm + 16 j + l % 16
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    // one m sub-tile's accumulators at a time: they count as written here, so
-    // their reads cannot move above the previous sub-tile's stores
-    asm volatile("" : "+a"(acc[0][j]), "+a"(acc[1][j]), "+a"(acc[2][j]), "+a"(acc[3][j]) :: "memory");
-    const int m = m0 + wm + 32 * j + r;
+  for (int j = 0; j < 8; ++j) {
+    asm volatile("" : "+a"(acc[0][j]), "+a"(acc[1][j]), "+a"(acc[2][j]), "+a"(acc[3][j]),
+                 "+a"(acc[4][j]), "+a"(acc[5][j]), "+a"(acc[6][j]), "+a"(acc[7][j]) :: "memory");
+    const int m = m0 + wm + 16 * j + r16;
     if (m >= M) continue;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int n = n0 + wn + 32 * i + 8 * q4 + 4 * hh;
-        if (n >= N) continue;                      // N is a multiple of 8: whole group in or out
-        const int64_t o = (int64_t)m * N + n;
-        f32x4 v = {acc[i][j][4 * q4 + 0], acc[i][j][4 * q4 + 1], acc[i][j][4 * q4 + 2],
-                   acc[i][j][4 * q4 + 3]};
-        if (R) {
-          const u32x2 rb = *(const u32x2*)(R + o);
-          v[0] += bf16_to_f32((uint16_t)(rb[0] & 0xFFFF));
-          v[1] += bf16_to_f32((uint16_t)(rb[0] >> 16));
-          v[2] += bf16_to_f32((uint16_t)(rb[1] & 0xFFFF));
-          v[3] += bf16_to_f32((uint16_t)(rb[1] >> 16));
-        }
-        *(bf16x4*)(Y + o) = __builtin_convertvector(v, bf16x4);
+    for (int i = 0; i < 8; ++i) {
+      const int n = n0 + wn + 16 * i + 4 * g4;
+      if (n >= N) continue;
+      const int64_t o = (int64_t)m * N + n;
+      f32x4 v = acc[i][j];
+      if (R) {
+        const u32x2 rb = *(const u32x2*)(R + o);
+        v[0] += bf16_to_f32((uint16_t)(rb[0] & 0xFFFF));
+        v[1] += bf16_to_f32((uint16_t)(rb[0] >> 16));
+        v[2] += bf16_to_f32((uint16_t)(rb[1] & 0xFFFF));
+        v[3] += bf16_to_f32((uint16_t)(rb[1] >> 16));
       }
+      *(bf16x4*)(Y + o) = __builtin_convertvector(v, bf16x4);
+    }
   }
 }
 

@@ -65,8 +65,9 @@ def test_gemm_rows_are_independent_and_deterministic():
 
 
 def test_gemm_tile_shapes_agree_bitwise():
-    """A product large enough for the 256 x 256 tiles (16 x 16 of them) and a
-    slice of its rows, which runs the 128 x 128 tiles: same bits per row."""
+    """A product large enough for the one-wave-per-SIMD kernel (16 x 16 tiles
+    of 256 x 256) and a slice of its rows, which runs the register-staged
+    kernel's 128 x 128 tiles: same bits per row."""
     from paper_2609_04875_amd import gemm_bf16
     rng = np.random.default_rng(5)
     x = _bf16_dev(rng.standard_normal((4096, 1024)))
