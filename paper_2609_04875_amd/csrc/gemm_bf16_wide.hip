@@ -1,7 +1,8 @@
 // Dense bf16 projection Y = X W^T (+ R), large-product path: one wave per
-// SIMD, each owning a 128 x 128 block of a 256 x 256 output tile, the 256
-// accumulators in AGPRs, X and W tiles brought to LDS by global->LDS loads,
-// and every K step laid out as 64 fenced issue slots.
+// SIMD, each owning a 128 x 128 block of a 256 x 256 output tile (8 x 8
+// sub-tiles of 16 x 16, 256 accumulators in AGPRs), X and W tiles brought to
+// LDS by global->LDS loads, and every K step laid out as 128 fenced issue
+// slots.
 //
 // K advances 64 at a time.  A step needs a 256 x 64 tile of X and one of W
 // (32 KB each, one 64 KB LDS buffer); two buffers alternate.  A wave
@@ -12,17 +13,19 @@
 // c ^ ((j / 2) mod 8), which spreads the 16 rows an operand read touches
 // over all 64 banks.
 //
-// Step schedule (slot s = one v_mfma_f32_32x32x16_bf16: k slice s / 16, W
-// sub-tile (s / 4) mod 4, X sub-tile s mod 4; each slice's 8 operands in a
-// register set of their own).  Slots 0-23 read slices 1-3 of this step, one
-// operand per slot.  At slot 24 the wave waits for its requests of step
-// kt + 1 (issued from slot 24 of the previous step on) and its LDS reads,
-// and the workgroup meets at the step's one barrier: step kt + 1's tiles are
-// then in LDS and every wave has read all of step kt's buffer.  Slots 24-39
-// read slice 0 of step kt + 1, and slots 24-54 issue this step's 16 requests
-// (step kt + 2, into the buffer just read), one every other slot, so that
-// the four waves' loads reach the CU's load path spread over the step.  The
-// loop is unrolled by two, so each buffer's operand addresses are
+// Step schedule (slot s = one v_mfma_f32_16x16x32_bf16: k slice s / 64, W
+// sub-tile (s / 8) mod 8, X sub-tile s mod 8; each slice's 16 operands in a
+// register set of their own).  Slots 0-31 read slice 1 of this step, one
+// operand every other slot.  At slot 40 the wave waits for its requests of
+// step kt + 1 (issued in slots 40-100 of the previous step) and its LDS
+// reads, and the workgroup meets at the step's one barrier: step kt + 1's
+// tiles are then in LDS and every wave has read all of step kt's buffer.
+// Slots 40-100 issue this step's 16 requests (step kt + 2, into the buffer
+// just read), one every fourth slot, so that the four waves' loads reach the
+// CU's load path spread over the step; slots 64-94 read slice 0 of step
+// kt + 1 (after the last product that reads slice 0 of this step).  Every
+// operand register is rewritten at least ten slots after its last reader.
+// The loop is unrolled by two, so each buffer's operand addresses are
 // loop-invariant registers plus immediates.  The loop issues no other
 // vector memory operation, so the vmcnt count is exact.
 //
@@ -36,7 +39,7 @@
 //
 // Every output element is accumulated by the same products in the same
 // order as in the register-staged kernel (A = W rows, B = X rows, k slices of
-// 16 from 0), so both give identical bits and rows of Y do not depend on the
+// 32 from 0), so both give identical bits and rows of Y do not depend on the
 // launch.
 #include <hip/hip_runtime.h>
 
@@ -124,8 +127,9 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
                  :: "v"(q < 8 ? xoff[q & 7] : woff[q & 7]), "s"(src), "s"(img) : "memory", "m0");
   };
 
-  // 16x16x32 products: operand = 16 rows x 32 k; lane l -> row l % 16, k
-  // group l / 16 (8 values), i.e. chunk 4 ks + l / 16 of the row
+  // Operand reads: 16 rows x 32 k (slice ks) of rows base + r16, lane l ->
+  // row l % 16, k group l / 16 (8 values): chunk 4 ks + l / 16 of the row,
+  // at slot (4 ks + l / 16) ^ gsw(r16) (every base is a multiple of 16)
   const int r16 = lane & 15, g4 = lane >> 4;
   int soff[2];
 #pragma unroll
@@ -140,12 +144,13 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
     else wa[ks][u >> 1] = v;
   };
 
-  f32x4 acc[8][8];      // [n sub-tile][m sub-tile]
+  f32x4 acc[8][8];      // [n sub-tile][m sub-tile], element (n, m)
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{};
 
+  // prologue: steps 0 and 1 requested, step 0 landed, its slice-0 operands read
 #pragma unroll
   for (int q = 0; q < 16; ++q) request(0, q);
 #pragma unroll
@@ -154,12 +159,19 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
 #pragma unroll
   for (int u = 0; u < 16; ++u) read_op(0, 0, u);
 
+  // step kt with its buffer parity CUR known at compile time, so that every
+  // operand address is a loop-invariant register plus an immediate
   auto step = [&](auto cur_c, int kt) {
     constexpr int cur = decltype(cur_c)::value, nxt = 1 - cur;
     auto slot = [&](auto ic) {
       constexpr int s = decltype(ic)::value;
       constexpr int ks = s / 64, i = (s / 8) % 8, j = s % 8;
-      if constexpr (s == 40) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if constexpr (s == 40) {
+        // step kt + 1 landed (this wave's requests, and the barrier for the
+        // other waves'), and every wave has read all of step kt's buffer,
+        // which the requests below refill with step kt + 2
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      }
       if constexpr (s < 32 && s % 2 == 0) read_op(cur, 1, s / 2);
       else if constexpr (s >= 64 && s < 96 && s % 2 == 0) read_op(nxt, 0, (s - 64) / 2);
       if constexpr (s >= 40 && s < 104 && s % 4 == 0) request(kt + 2, (s - 40) / 4);
@@ -174,12 +186,16 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
     step(std::integral_constant<int, 1>{}, kt + 1);
   }
   if (kt < nk) step(std::integral_constant<int, 0>{}, kt);
+  // 19 wait states before any VALU read of the accumulators (the epilogue
+  // reads each m sub-tile's after an assembly statement ordered after this)
   asm volatile("s_nop 15\n\ts_nop 3" ::: "memory");
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // requests past the end, before LDS is handed on
 
   // acc[i][j] lane l, register q: n = wn + 16 i + 4 (l / 16) + q, m = wm + 16 j + l % 16
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
+    // one m sub-tile's accumulators at a time: they count as written here, so
+    // their reads cannot move above the previous sub-tile's stores
     asm volatile("" : "+a"(acc[0][j]), "+a"(acc[1][j]), "+a"(acc[2][j]), "+a"(acc[3][j]),
                  "+a"(acc[4][j]), "+a"(acc[5][j]), "+a"(acc[6][j]), "+a"(acc[7][j]) :: "memory");
     const int m = m0 + wm + 16 * j + r16;
@@ -187,7 +203,7 @@ gemm_bf16_wide_kernel(int M, int N, int K, const uint16_t* __restrict__ X,
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int n = n0 + wn + 16 * i + 4 * g4;
-      if (n >= N) continue;
+      if (n >= N) continue;                        // N is a multiple of 8: whole group in or out
       const int64_t o = (int64_t)m * N + n;
       f32x4 v = acc[i][j];
       if (R) {
