@@ -68,7 +68,7 @@ constexpr int kGNB = 2;                // LDS buffers
 constexpr int kGImg = kGB * kGK;       // elements of one X or W image
 constexpr int kGBuf = 2 * kGImg;       // elements of one buffer (X image, then W image)
 constexpr int kGRuns = 8;              // 1 KB runs per wave and image per step
-constexpr int kGGroupM = 8;            // tile rows per group of the tile order
+constexpr int kGGroupM = 4;            // tile rows per group of the tile order
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
