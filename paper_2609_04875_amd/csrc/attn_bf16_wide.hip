@@ -47,14 +47,20 @@
 //
 // Step schedule.  Tiles whose keys all precede the workgroup's first query
 // need no mask.  Step t is 64 issue slots fenced by sched_barrier, one product
-// each: slots 0-31 the products of S(t+1), slots 32-63 O += V(t) P(t); around
-// them the eight requests of tile t+3 (slots 0-7), LDS operand reads two
-// operands ahead, the exponentials of P(t) (two per item, their bf16
-// rounding two slots later) and the row max of S(t+1) (slots 34-63, after
-// its last product).  A single wave has no partner wave to fill the matrix
-// pipe while it waits, so the order is fixed here rather than left to the
-// scheduler.  Tiles that straddle the diagonal run unpipelined with the mask
-// applied by select; a tile past kv_len gets its V^T slots zeroed in LDS.
+// each: slots 0-3 the last four products of O += V(t-1) P(t-1), deferred
+// from the step before so that the matrix pipe has work while the first K
+// operands of this step come from LDS (they can only be read after the
+// step's barrier); slots 4-35 the products of S(t+1); slots 36-63 the first
+// 28 products of O += V(t) P(t).  Around them: the eight requests of tile
+// t+3 (slots 0-7), LDS operand reads two operands ahead, the exponentials of
+// P(t) (two per item, their bf16 rounding two slots later) and the row max
+// of S(t+1) (slots 38-63, after its last product).  Every O accumulator
+// still receives its products in the same order; when a row moves its
+// reference max, the deferred products are issued before O is rescaled.  A
+// single wave has no partner wave to fill the matrix pipe while it waits,
+// so the order is fixed here rather than left to the scheduler.  Tiles that
+// straddle the diagonal run unpipelined with the mask applied by select; a
+// tile past kv_len gets its V^T slots zeroed in LDS.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -77,6 +83,12 @@ constexpr int kWKT = 64;            // keys per tile
 constexpr int kWBufElems = 16384;   // elements per LDS tile buffer (K 8192, V^T 8192)
 constexpr float kWSlack = 8.f;      // lazy rescale threshold, log2 units
 constexpr int kWMaxIdt = 8192;      // block-table entries a workgroup keeps in LDS
+// products of O += V P deferred past the next step's barrier (0, 2, 4, 6 or
+// 8; 4 and 8 measured alike, both 1% faster than none)
+#ifndef PGSR_WIDE_DEFER
+#define PGSR_WIDE_DEFER 4
+#endif
+constexpr int kWDefer = PGSR_WIDE_DEFER;
 
 // f(integral_constant<int, I>) for I = 0, 1, ... in order, at compile time.
 template <class F, int... I>
@@ -287,24 +299,61 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       mx[b] = fmaxf(x, xor32(x)) + m_use[b];   // S holds s * c - m_use
     }
   };
-  auto apply_max = [&](const float (&mx)[QB], f32x16 (&st)[QB][2]) {
+  // The last kWDefer products of O += V(t) P(t) (16-key step 3) are issued
+  // after the next step's barrier, so that they keep the matrix pipe busy
+  // while the first operands of that step are read from LDS; their V^T
+  // operands and P stay in registers until then.  Each accumulator still
+  // receives its products in the same order.  Before zero: no pending work.
+  constexpr int ND = kWDefer;
+  static_assert(ND % 2 == 0 && ND >= 0 && ND <= 8, "deferred products");
+  bf16x8 dv[ND > 0 ? ND / 2 : 1];
+  u32x4 dp[QB];
+#pragma unroll
+  for (int k = 0; k < (ND > 0 ? ND / 2 : 1); ++k) dv[k] = bf16x8{};
+#pragma unroll
+  for (int b = 0; b < QB; ++b) dp[b] = u32x4{0, 0, 0, 0};
+  auto deferred = [&](auto kc) {
+    constexpr int k = decltype(kc)::value;       // product k of the deferred ones
+    constexpr int j = 32 - ND + k, db = (j / 2) % 4, b = j % 2;
+    // the first may follow right after VALU writes of dv / dp
+    if constexpr (k == 0) asm volatile("s_nop 1");
+    mfma_o(dv[k / 2], __builtin_bit_cast(bf16x8, dp[b]), oacc[b][db]);
+  };
+  auto deferred_all = [&]() {
+    if constexpr (ND > 0) static_for(deferred, std::make_integer_sequence<int, ND>{});
+  };
+
+  // New reference max per row; when any row of the wave moves it, rescale O
+  // (after the deferred products when flush is set; they are then issued
+  // here and zeroed, so that the next step adds nothing with them).
+  auto apply_max = [&](const float (&mx)[QB], f32x16 (&st)[QB][2], auto flush) {
     bool any = false;
-    float delta[QB];
+    bool bump[QB];
+    float delta[QB], m_old[QB];
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      const bool bump = mx[b] > m[b] + kWSlack;
-      const float m_new = bump ? mx[b] : m[b];
+      bump[b] = mx[b] > m[b] + kWSlack;
+      const float m_new = bump[b] ? mx[b] : m[b];
       const float mu = m_new == -INFINITY ? 0.f : m_new;
       delta[b] = mu - m_use[b];
+      m_old[b] = m[b];
       m_use[b] = mu;
-      alpha[b] = bump ? __builtin_amdgcn_exp2f(m[b] - m_use[b]) : 1.f;
+      alpha[b] = 1.f;
       m[b] = m_new;
-      any = any || bump;
+      any = any || bump[b];
     }
     if (__ballot(any)) {
+      if constexpr (decltype(flush)::value) deferred_all();
       oacc_sync(true);
+      if constexpr (decltype(flush)::value && ND > 0) {
+#pragma unroll
+        for (int k = 0; k < ND / 2; ++k) dv[k] = bf16x8{};
+#pragma unroll
+        for (int b = 0; b < QB; ++b) dp[b] = u32x4{0, 0, 0, 0};
+      }
 #pragma unroll
       for (int b = 0; b < QB; ++b) {
+        alpha[b] = bump[b] ? __builtin_amdgcn_exp2f(m_old[b] - m_use[b]) : 1.f;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) oacc[b][db] *= alpha[b];
         st[b][0] -= delta[b];
@@ -319,7 +368,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   auto update_max = [&](f32x16 (&s)[QB][2]) {
     float mx[QB];
     row_max(s, mx);
-    apply_max(mx, s);
+    apply_max(mx, s, std::false_type{});
   };
   // P for 16 keys (registers o8 .. o8+7 of one 32-key half), rounded to bf16,
   // with the row-sum terms added in the fixed order.
@@ -415,6 +464,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   // ---- pipelined steps over unmasked tiles ----------------------------- //
   auto step = [&](int t, const f32x16 (&sc)[QB][2], f32x16 (&sn)[QB][2]) {
     constexpr int kPF = 2;                      // operands read ahead
+    constexpr int NU = 32 - ND / 2;             // operands of this step's own products
     bar();
     int ids[KB];
 #pragma unroll
@@ -427,36 +477,55 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       ps[b][0] = ps[b][1] = 0.f;
       mxa[b] = -INFINITY;
     }
-    bf16x8 opnd[32];                            // 16 K then 16 V^T operands
+    // operand u (16 K, then the V^T operands of the products issued in this
+    // step) feeds the products of slots ND + 2u and ND + 2u + 1
+    bf16x8 opnd[NU];
+    bf16x8 dvn[ND > 0 ? ND / 2 : 1];            // V^T operands of the products deferred to the next step
     u32x4 idv;                                  // block offsets of tile t + 4
     f32x2 ex[4];                                // exponentials awaiting their rounding
     auto read_op = [&](int u) {
       opnd[u] = u < 16 ? k_op(tk, u % 2, u / 2) : v_op(tv, (u - 16) / 4, (u - 16) % 4);
     };
 #pragma unroll
-    for (int u = 0; u < kPF; ++u) read_op(u);
+    for (int u = 0; u < kPF - ND / 2; ++u) read_op(u);
     auto slot = [&](auto ic) {
       constexpr int i = decltype(ic)::value;
       if constexpr (i < 8) request(tr, ids, i);
-      if constexpr (i % 2 == 0 && i / 2 + kPF < 32) read_op(i / 2 + kPF);
-      if constexpr (i < 32) {
-        constexpr int ds = i / 4, kh = (i / 2) % 2, b = i % 2;
-        if constexpr (ds == 0) sn[b][kh] = mfma_s0(opnd[i / 2], qf[b][ds], cinit[b]);
-        else mfma_s(opnd[i / 2], qf[b][ds], sn[b][kh]);
+      if constexpr (i % 2 == 0) {
+        constexpr int u = (i - ND) / 2 + kPF;
+        if constexpr (u >= 0 && u < NU) read_op(u);
+      }
+      if constexpr (ND > 0 && i >= 64 - ND && (i - (64 - ND)) % 2 == 0) {
+        constexpr int k = (i - (64 - ND)) / 2, j = 32 - ND + 2 * k;
+        dvn[k] = v_op(tv, j / 8, (j / 2) % 4);
+      }
+      if constexpr (i < ND) {
+        deferred(ic);
+      } else if constexpr (i < ND + 32) {
+        constexpr int q = i - ND, ds = q / 4, kh = (q / 2) % 2, b = q % 2;
+        if constexpr (ds == 0) sn[b][kh] = mfma_s0(opnd[q / 2], qf[b][ds], cinit[b]);
+        else mfma_s(opnd[q / 2], qf[b][ds], sn[b][kh]);
       } else {
-        constexpr int j = i - 32, ks = j / 8, db = (j / 2) % 4, b = j % 2;
+        constexpr int j = i - ND - 32, ks = j / 8, db = (j / 2) % 4, b = j % 2;
         // the last pair of P(t) for (b, ks) was rounded at least 3 slots
         // earlier (item placement below): past the VALU -> matrix wait states
-        mfma_o(opnd[i / 2], __builtin_bit_cast(bf16x8, pw[b][ks]), oacc[b][db]);
+        mfma_o(opnd[16 + j / 2], __builtin_bit_cast(bf16x8, pw[b][ks]), oacc[b][db]);
       }
-      if constexpr (i == 33) s_sync(sn);
+      if constexpr (i == ND + 33) s_sync(sn);
       if constexpr (i == 40) idv = ids_fetch(t + 4);
       // keep the operand of slots i-3 and i-2 allocated until here, so that
       // no VALU result lands in registers a product may still be reading
-      if constexpr (i >= 3 && (i - 3) % 2 == 0) asm volatile("" ::"v"(opnd[(i - 3) / 2]));
+      if constexpr (i >= 3) {
+        constexpr int pp = i - 3;
+        if constexpr (pp < ND) {
+          if constexpr (pp % 2 == 0) asm volatile("" ::"v"(dv[pp / 2]));
+        } else if constexpr ((pp - ND) % 2 == 0) {
+          asm volatile("" ::"v"(opnd[(pp - ND) / 2]));
+        }
+      }
       // key pairs of P(t): item w = (ks, m, b) in ks-major order; its two
       // exponentials at slot floor(52 w / 32), their bf16 rounding two slots
-      // later, so p[b][ks] is complete three slots before slot 32 + 8 ks
+      // later, so p[b][ks] is complete three slots before its first product
       constexpr int we = (32 * i + 51) / 52;
       if constexpr (we < 32 && (we * 52) / 32 == i) {
         constexpr int ks = we / 8, mm = (we / 2) % 4, b = we % 2;
@@ -468,17 +537,18 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
         constexpr int ks = wc / 8, mm = (wc / 2) % 4, b = wc % 2;
         pw[b][ks][mm] = __builtin_bit_cast(uint32_t, __builtin_convertvector(ex[wc % 4], bf16x2));
       }
-      // row max of S(t+1): 32 v_max3 items at slots 34 + floor(30 w / 32),
-      // as inline assembly (S comes from inline assembly, so fmaxf would
-      // first quiet every input)
-      if constexpr (i >= 34) {
-        constexpr int w0 = (32 * (i - 34) + 29) / 30;
-        if constexpr (w0 < 32 && 34 + (w0 * 30) / 32 == i) {
+      // row max of S(t+1): 32 v_max3 items spread over the slots after its
+      // last product and the wait for its results, as inline assembly (S
+      // comes from inline assembly, so fmaxf would first quiet every input)
+      constexpr int MB = ND + 34, MS = 64 - MB;
+      if constexpr (i >= MB) {
+        constexpr int w0 = (32 * (i - MB) + MS - 1) / MS;
+        if constexpr (w0 < 32 && MB + (w0 * MS) / 32 == i) {
           constexpr int b = w0 % 2, q = w0 / 2, kh = q / 8, o = 2 * (q % 8);
           asm("v_max3_f32 %0, %0, %1, %2" : "+v"(mxa[b]) : "v"(sn[b][kh][o]), "v"(sn[b][kh][o + 1]));
         }
         constexpr int w1 = w0 + 1;
-        if constexpr (w1 < 32 && 34 + (w1 * 30) / 32 == i) {
+        if constexpr (w1 < 32 && MB + (w1 * MS) / 32 == i) {
           constexpr int b = w1 % 2, q = w1 / 2, kh = q / 8, o = 2 * (q % 8);
           asm("v_max3_f32 %0, %0, %1, %2" : "+v"(mxa[b]) : "v"(sn[b][kh][o]), "v"(sn[b][kh][o + 1]));
         }
@@ -506,7 +576,13 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
       // sink both unrolled steps' sums to the loop's end)
       asm volatile("" ::"v"(l[b]));
     }
-    apply_max(mx, sn);
+    if constexpr (ND > 0) {
+#pragma unroll
+      for (int k = 0; k < ND / 2; ++k) dv[k] = dvn[k];
+#pragma unroll
+      for (int b = 0; b < QB; ++b) dp[b] = pw[b][NKS - 1];
+    }
+    apply_max(mx, sn, std::true_type{});
   };
   // Request tile x + 3 with the ids taken a step ago, take the next ids.
   auto advance = [&](int x) {
@@ -520,6 +596,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   auto finish = [&](int t, const f32x16 (&sc)[QB][2]) {
     bar();
     advance(t);
+    deferred_all();
     pv_tile(buf_of(t), sc);
   };
   // A tile on the diagonal: S, causal mask by select, max, then P V.
