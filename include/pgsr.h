@@ -15,7 +15,8 @@
  *
  * Memory model.  Every device pointer is owned by the caller (allocated, e.g.,
  * as torch tensors), must stay valid for the pool's lifetime and is never
- * freed or reallocated here.  The library allocates no device memory.  It keeps
+ * freed or reallocated here.  The library allocates no device memory (the
+ * checked build below: one 4-byte flag per pool, at pool creation).  It keeps
  * a HOST mirror of per-sequence length and block count and of the free-list
  * top, updated at call time in enqueue order; one pool must not be used from
  * two host threads at once.
@@ -41,6 +42,16 @@
  * nor device state changed.  PGSR_EHIP means a HIP call failed after
  * validation; device state is then undefined and the pool must be re-created.
  * pgsr_last_error() describes the most recent failure on the calling thread.
+ *
+ * Checked build.  The same sources compiled with PGSR_CHECKED
+ * (lib/libpgsr_checked.so, same ABI) validate on the device every block id
+ * they read from block_tables or free_list before it addresses the cache, the
+ * counts or the stack.  Only device metadata written behind the library's back
+ * can hold an id outside [0, n_blocks); the checked build then uses block 0
+ * instead, finishes the call's launches, waits for them, and returns
+ * PGSR_ERANGE from pgsr_kv_crop, pgsr_kv_fork and the prefill calls (device
+ * state is then undefined, as after PGSR_EHIP).  Because of that wait, its
+ * calls synchronise the stream; it is a debugging aid, not the fast path.
  *
  * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Every call
  * only enqueues work and returns without synchronising, except

@@ -3,6 +3,12 @@
 Each source is compiled with hipcc to an object under ``_build/`` and the
 objects are linked into ``paper_2609_04875_amd/lib/libpgsr.so``.  Packed fp32
 instructions are disabled for all device code (-packed-fp32-ops).
+
+``build_all`` also links the checked build, ``lib/libpgsr_checked.so``: the
+same sources with PGSR_CHECKED, whose kernels validate every block id they
+read from the block table or the free stack and whose pool calls then return
+PGSR_ERANGE instead of touching memory outside the pool (a debugging aid for
+device metadata written outside the library; same C ABI).
 """
 from __future__ import annotations
 
@@ -19,6 +25,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build", "pgsr")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libpgsr.so")
+CHECKED_LIB = os.path.join(LIBDIR, "libpgsr_checked.so")
 ARCH = os.environ.get("PGSR_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -73,5 +80,10 @@ def build(verbose: bool = False, lib: str = LIB, defines=()) -> str:
     return lib
 
 
+def build_all(verbose: bool = False) -> tuple:
+    """The default library and the checked build."""
+    return build(verbose), build(verbose, lib=CHECKED_LIB, defines=("PGSR_CHECKED",))
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(*build_all(verbose="-v" in sys.argv), sep="\n")

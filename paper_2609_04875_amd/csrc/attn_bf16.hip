@@ -167,7 +167,9 @@ attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_t*
   // issued ahead of that tile's data loads so waiting for the data implies
   // they have arrived, then broadcast to scalar registers with readlane.
   int idv = 0;
-  auto fetch_ids = [&](int kt) { idv = row[min(kt * KB + (lane < KB ? lane : 0), last_blk)]; };
+  auto fetch_ids = [&](int kt) {
+    idv = blk_id(row[min(kt * KB + (lane < KB ? lane : 0), last_blk)], a.n_blocks, a.chk);
+  };
   auto take_ids = [&]() {
     Ids ids;
     ids.v0 = __builtin_amdgcn_readlane(idv, 0);

@@ -161,7 +161,9 @@ attn_bf16_pipe_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   // step ahead; each chunk reads its block's id with readlane at a scalar
   // lane index.
   int idv = 0;
-  auto fetch_ids = [&](int kt) { idv = row[min(kt * KB + (lane < KB ? lane : 0), last_blk)]; };
+  auto fetch_ids = [&](int kt) {
+    idv = blk_id(row[min(kt * KB + (lane < KB ? lane : 0), last_blk)], a.n_blocks, a.chk);
+  };
   // Per-lane element offsets of a thread's chunks inside a block-head (K:
   // slot-major rows of D; V: d-major rows of B slots), fixed for the kernel;
   // a load is then a scalar block pointer plus this offset.

@@ -173,7 +173,9 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   const uint32_t blk_bytes = (uint32_t)hkv * (B * D * 2);
   auto tile_ids_s = [&](int kt, int (&id)[KB]) {
 #pragma unroll
-    for (int j = 0; j < KB; ++j) id[j] = (int)((uint32_t)row[min(kt * KB + j, last_blk)] * blk_bytes);
+    for (int j = 0; j < KB; ++j)
+      id[j] = __builtin_amdgcn_readfirstlane(
+          (int)((uint32_t)blk_id(row[min(kt * KB + j, last_blk)], a.n_blocks, a.chk) * blk_bytes));
   };
   // The workgroup's block offsets (blocks kt0 * KB .. last_blk) in LDS, so
   // that the loop takes its block ids with LDS reads (in order with the
@@ -182,7 +184,7 @@ attn_bf16_wide_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint
   // Entries past last_blk repeat it (tiles up to n_kt + 3 are requested).
   const int blk0 = kt0 * KB;
   for (int i = tid; i < (n_kt + 4 - kt0) * KB; i += NW * 64)
-    idt[i] = (uint32_t)row[min(blk0 + i, last_blk)] * blk_bytes;
+    idt[i] = (uint32_t)blk_id(row[min(blk0 + i, last_blk)], a.n_blocks, a.chk) * blk_bytes;
   auto ids_fetch = [&](int kt) { return *(const u32x4*)&idt[(kt - kt0) * KB]; };
   auto ids_use = [&](const u32x4& v, int (&id)[KB]) {
 #pragma unroll

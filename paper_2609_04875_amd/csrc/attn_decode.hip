@@ -115,8 +115,8 @@ attn_decode_kernel(AttnArgs a, const int32_t* __restrict__ tables, const uint16_
     const int k0 = kb + 16 * hh;
     return k0 < kv_len ? k0 : ((kv_len - 1) & ~15);
   };
-  auto k_id = [&](int kb) { return row[k_key(kb) / B]; };
-  auto v_id = [&](int kb) { return row[v_key(kb) / B]; };
+  auto k_id = [&](int kb) { return blk_id(row[k_key(kb) / B], a.n_blocks, a.chk); };
+  auto v_id = [&](int kb) { return blk_id(row[v_key(kb) / B], a.n_blocks, a.chk); };
 
   u32x4 kr[NK], vr[NV];
   auto load_k = [&](int kb, int idk) {

@@ -95,7 +95,7 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
       const int pos = kb + j;
       f32x4 val = {0, 0, 0, 0};
       if (pos < kv_len) {
-        const int32_t id = row[pos / B];
+        const int32_t id = blk_id(row[pos / B], a.n_blocks, a.chk);
         val = *(const f32x4*)(kc + ((layer_off + (int64_t)id * a.n_kv_heads + g) * B + pos % B) * D + c);
       }
       *(f32x4*)(ks + j * D + c) = val;
@@ -106,7 +106,7 @@ __global__ void __launch_bounds__(kWaves * 64) attn_f32_kernel(AttnArgs a) {
       const int pos = kb + j;                    // 4 slots of one block (B % 4 == 0)
       f32x4 val = {0, 0, 0, 0};
       if (pos < kv_len) {
-        const int32_t id = row[pos / B];
+        const int32_t id = blk_id(row[pos / B], a.n_blocks, a.chk);
         val = *(const f32x4*)(vc + ((layer_off + (int64_t)id * a.n_kv_heads + g) * D + c) * B + pos % B);
 #pragma unroll
         for (int r = 1; r < 4; ++r)

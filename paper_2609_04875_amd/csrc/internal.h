@@ -15,6 +15,28 @@ namespace pgsr {
 
 constexpr int kMaxSeqsPerLaunch = 64;
 
+// ------------------------------------------------------- checked build --- //
+// A library built with -DPGSR_CHECKED validates every block id it reads from
+// the block table or the free stack before the id addresses the cache, the
+// counts or the stack: an id outside [0, n_blocks) is replaced by block 0 and
+// recorded in *chk (a device word the pool owns), and the call returns
+// PGSR_ERANGE once its launches have finished.  Only memory written behind
+// the library's back can hold such an id (the host mirror validates every
+// call), so the default build reads ids unchecked; the checked one turns that
+// corruption into an error instead of an access outside the pool.
+__device__ __forceinline__ int32_t blk_id(int32_t id, int32_t n_blocks, int32_t* chk) {
+#ifdef PGSR_CHECKED
+  if ((uint32_t)id >= (uint32_t)n_blocks) {
+    atomicOr(chk, 1);
+    return 0;
+  }
+#else
+  (void)n_blocks;
+  (void)chk;
+#endif
+  return id;
+}
+
 // ---------------------------------------------------------------- crop ---- //
 struct CropEntry {
   int32_t seq;       // row of the block table
@@ -33,7 +55,8 @@ struct CropArgs {
   int32_t* free_list;
   int32_t* free_top;
   int32_t* refs;
-  int32_t max_bps;
+  int32_t* chk;        // checked build: out-of-range block id seen
+  int32_t max_bps, n_blocks;
   int32_t top_before;  // stack height when this launch starts
   int32_t n;
   CropEntry e[kMaxSeqsPerLaunch];
@@ -47,6 +70,7 @@ struct PoisonArgs {
   void* v_cache;
   const int32_t* tables;
   const int32_t* free_list;
+  int32_t* chk;
   int32_t max_bps, n_layers, n_blocks, n_kv_heads, block_size, head_dim, elem_bytes;
   int32_t top_before;
   int32_t n_freed;
@@ -65,7 +89,8 @@ struct ForkArgs {
   int32_t* tables;
   int32_t* lens;
   int32_t* refs;
-  int32_t max_bps;
+  int32_t* chk;
+  int32_t max_bps, n_blocks;
   int32_t n;
   ForkEntry e[kMaxSeqsPerLaunch];
 };
@@ -94,6 +119,7 @@ struct AppendArgs {
   const int32_t* free_list;
   int32_t* free_top;
   int32_t* refs;
+  int32_t* chk;
   int32_t max_bps, n_blocks, n_kv_heads, block_size, head_dim, layer, n_layers;
   int32_t commit;
   // FP8 E4M3 cache (1-byte elements) fed from bf16 inputs: each value is stored
@@ -125,6 +151,7 @@ struct FusedAppendArgs {
   int32_t* free_list;
   int32_t* free_top;
   int32_t* refs;
+  int32_t* chk;
   int32_t max_bps, n_blocks, n_kv_heads, block_size, head_dim, layer;
   int32_t commit;
   int32_t top_before;  // stack height before the crop
@@ -152,6 +179,7 @@ struct AttnArgs {
   const void* k_cache;
   const void* v_cache;
   const int32_t* tables;
+  int32_t* chk;
   int32_t max_bps, n_blocks, n_q_heads, n_kv_heads, block_size, head_dim, layer;
   float scale_log2;    // softmax_scale * log2(e) (times the K scale of an FP8 cache)
   float o_scale;       // output factor: the V scale of an FP8 cache, else 1

@@ -51,7 +51,7 @@ __global__ void __launch_bounds__(256) crop_kernel(CropArgs a) {
       bool freed = false;
       int32_t b = -1;
       if (j < e.nalloc) {
-        b = row[j];
+        b = blk_id(row[j], a.n_blocks, a.chk);
         row[j] = -1;
         const int32_t r = a.refs[b] - 1;
         a.refs[b] = r;
@@ -79,7 +79,7 @@ __global__ void __launch_bounds__(256) fork_kernel(ForkArgs a) {
   const int32_t* src = a.tables + (int64_t)e.src * a.max_bps;
   int32_t* dst = a.tables + (int64_t)e.dst * a.max_bps;
   for (int32_t j = threadIdx.x; j < e.nalloc; j += blockDim.x) {
-    const int32_t b = src[j];
+    const int32_t b = blk_id(src[j], a.n_blocks, a.chk);
     dst[j] = b;
     atomicAdd(&a.refs[b], 1);
   }
@@ -101,7 +101,7 @@ __global__ void __launch_bounds__(256) poison_kernel(PoisonArgs a, T nan) {
   T* kc = (T*)a.k_cache + (int64_t)layer * a.n_blocks * blk_elems;
   T* vc = (T*)a.v_cache + (int64_t)layer * a.n_blocks * blk_elems;
   if ((int)blockIdx.x < a.n_freed) {
-    const int32_t id = a.free_list[a.top_before + blockIdx.x];
+    const int32_t id = blk_id(a.free_list[a.top_before + blockIdx.x], a.n_blocks, a.chk);
     fill_nan(kc + (int64_t)id * blk_elems, blk_elems, nan, threadIdx.x, blockDim.x);
     fill_nan(vc + (int64_t)id * blk_elems, blk_elems, nan, threadIdx.x, blockDim.x);
     return;
@@ -109,7 +109,7 @@ __global__ void __launch_bounds__(256) poison_kernel(PoisonArgs a, T nan) {
   const CropEntry e = a.e[blockIdx.x - a.n_freed];
   const int32_t tail = e.new_len % a.block_size;
   if (tail != 0 && e.tail_private) {  // slots tail .. B-1 of the kept partial block
-    const int32_t id = a.tables[(int64_t)e.seq * a.max_bps + e.keep - 1];
+    const int32_t id = blk_id(a.tables[(int64_t)e.seq * a.max_bps + e.keep - 1], a.n_blocks, a.chk);
     const int B = a.block_size, D = a.head_dim;
     const int per_head = (B - tail) * D;
     for (int i = threadIdx.x; i < a.n_kv_heads * per_head; i += blockDim.x) {
@@ -132,7 +132,7 @@ __global__ void __launch_bounds__(256) cow_kernel(AppendArgs a) {
   const AppendEntry e = a.e[blockIdx.x];
   if (e.cow_old < 0) return;
   const int B = a.block_size, D = a.head_dim, h = blockIdx.y;
-  const int32_t id = a.free_list[e.stack_before - 1];
+  const int32_t id = blk_id(a.free_list[e.stack_before - 1], a.n_blocks, a.chk);
   const int s0 = e.prefix - e.lb_first * B;
   if (h == 0 && threadIdx.x == 0) {
     a.tables[(int64_t)e.seq * a.max_bps + e.lb_first] = id;
@@ -207,9 +207,9 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a) {
   const int32_t cow_pops = e.cow_old >= 0 ? 1 : 0;   // cow_kernel took the first pop
   int32_t id;
   if (lb < e.nalloc_before) {
-    id = row[lb];
+    id = blk_id(row[lb], a.n_blocks, a.chk);
   } else {
-    id = a.free_list[e.stack_before - 1 - cow_pops - (lb - e.nalloc_before)];
+    id = blk_id(a.free_list[e.stack_before - 1 - cow_pops - (lb - e.nalloc_before)], a.n_blocks, a.chk);
     if (h == 0 && threadIdx.x == 0) {
       row[lb] = id;
       a.refs[id] = 1;
@@ -370,9 +370,10 @@ __global__ void __launch_bounds__(64) append_bf16_kernel(AppendArgs a) {
   const int32_t p1 = min(e.prefix + e.q_len, (lb + 1) * B);
   int32_t* row = a.tables + (int64_t)e.seq * a.max_bps;
   const int32_t cow_pops = e.cow_old >= 0 ? 1 : 0;   // cow_kernel took the first pop
-  const int32_t id = lb < e.nalloc_before
-                         ? row[lb]
-                         : a.free_list[e.stack_before - 1 - cow_pops - (lb - e.nalloc_before)];
+  const int32_t id = blk_id(lb < e.nalloc_before
+                                 ? row[lb]
+                                 : a.free_list[e.stack_before - 1 - cow_pops - (lb - e.nalloc_before)],
+                             a.n_blocks, a.chk);
   if (h == 0 && lane == 0) {
     if (lb >= e.nalloc_before) {
       row[lb] = id;
@@ -418,7 +419,7 @@ __global__ void __launch_bounds__(64) fused_append_kernel(FusedAppendArgs a) {
 #pragma unroll
         for (int k = 0; k < R; ++k) {
           const int32_t j = j0 + 64 * k + lane;
-          b[k] = j < c.nalloc ? row[j] : -1;
+          b[k] = j < c.nalloc ? blk_id(row[j], a.n_blocks, a.chk) : -1;
         }
 #pragma unroll
         for (int k = 0; k < R; ++k) r[k] = b[k] >= 0 ? a.refs[b[k]] - 1 : 1;
@@ -446,7 +447,8 @@ __global__ void __launch_bounds__(64) fused_append_kernel(FusedAppendArgs a) {
 #pragma unroll
         for (int k = 0; k < R; ++k) {
           const int32_t lb = lb0 + 64 * k + lane;
-          id[k] = lb < end ? a.free_list[e.stack_before - 1 - (lb - e.nalloc_before)] : -1;
+          id[k] = lb < end ? blk_id(a.free_list[e.stack_before - 1 - (lb - e.nalloc_before)], a.n_blocks, a.chk)
+                           : -1;
         }
 #pragma unroll
         for (int k = 0; k < R; ++k) {

@@ -50,6 +50,9 @@ struct pgsr_pool {
   uint64_t* clk = nullptr;
   int32_t clk_n = 0;
   bool clk_written = false;
+  // checked build: device word the kernels set when a block id they read is
+  // out of range (null in the default build)
+  int32_t* chk = nullptr;
 };
 
 namespace {
@@ -73,6 +76,31 @@ int ok() {
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(PGSR_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// After a call's launches: in the checked build, wait for them and report a
+// block id that a kernel found out of range (the flag is cleared for the next
+// call); in the default build there is nothing to check.
+int device_check(pgsr_pool* p, hipStream_t st) {
+#ifdef PGSR_CHECKED
+  int32_t h = 0;
+  hipError_t err = hipMemcpyAsync(&h, p->chk, sizeof h, hipMemcpyDeviceToHost, st);
+  if (err == hipSuccess) err = hipStreamSynchronize(st);
+  if (err != hipSuccess) return hip_fail(err, "checked build: flag read");
+  if (h != 0) {
+    err = hipMemsetAsync(p->chk, 0, sizeof h, st);
+    if (err == hipSuccess) err = hipStreamSynchronize(st);
+    if (err != hipSuccess) return hip_fail(err, "checked build: flag reset");
+    return fail(PGSR_ERANGE,
+                "checked build: a kernel read a block id outside [0, %d) from the block table or the "
+                "free stack (device metadata written outside the library); block 0 was used instead",
+                p->n_blocks);
+  }
+#else
+  (void)p;
+  (void)st;
+#endif
+  return PGSR_OK;
 }
 
 inline int32_t cdiv(int64_t a, int64_t b) { return (int32_t)((a + b - 1) / b); }
@@ -160,7 +188,9 @@ int do_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_len
     a.free_list = p->free_list;
     a.free_top = p->free_top;
     a.refs = p->refs;
+    a.chk = p->chk;
     a.max_bps = p->max_bps;
+    a.n_blocks = p->n_blocks;
     a.top_before = p->h_top;
     a.n = cnt;
     for (int32_t i = 0; i < cnt; ++i) {
@@ -182,6 +212,7 @@ int do_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* new_len
       pa.v_cache = p->v_cache;
       pa.tables = p->tables;
       pa.free_list = p->free_list;
+      pa.chk = p->chk;
       pa.max_bps = p->max_bps;
       pa.n_layers = p->n_layers;
       pa.n_blocks = p->n_blocks;
@@ -308,6 +339,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.free_list = p->free_list;
     a.free_top = p->free_top;
     a.refs = p->refs;
+    a.chk = p->chk;
     a.max_bps = p->max_bps;
     a.n_blocks = p->n_blocks;
     a.n_kv_heads = p->hkv;
@@ -360,6 +392,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.free_list = p->free_list;
     a.free_top = p->free_top;
     a.refs = p->refs;
+    a.chk = p->chk;
     a.max_bps = p->max_bps;
     a.n_blocks = p->n_blocks;
     a.n_kv_heads = p->hkv;
@@ -443,6 +476,7 @@ int do_replay(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
     a.k_cache = p->k_cache;
     a.v_cache = p->v_cache;
     a.tables = p->tables;
+    a.chk = p->chk;
     a.max_bps = p->max_bps;
     a.n_blocks = p->n_blocks;
     a.n_q_heads = p->hq;
@@ -704,14 +738,25 @@ int pgsr_pool_create(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
     p->h_free[i] = init_free_order ? init_free_order[i] : n_blocks - 1 - i;
   p->h_ref.assign(n_blocks, 0);
   p->h_top = n_blocks;
+#ifdef PGSR_CHECKED
+  err = hipMalloc((void**)&p->chk, sizeof(int32_t));
+  if (err == hipSuccess) err = hipMemset(p->chk, 0, sizeof(int32_t));
+  if (err != hipSuccess) {
+    (void)hipFree(p->chk);
+    delete p;
+    return hip_fail(err, "checked build: flag allocation");
+  }
+#endif
   *out = p;
   return ok();
 }
 
 int pgsr_pool_destroy(pgsr_pool* pool) {
-  if (pool)
+  if (pool) {
     for (hipEvent_t& e : pool->ev)
       if (e) (void)hipEventDestroy(e);
+    if (pool->chk) (void)hipFree(pool->chk);
+  }
   delete pool;
   return ok();
 }
@@ -867,6 +912,7 @@ int pgsr_kv_crop(pgsr_pool* p, int32_t n, const int32_t* seqs, const int32_t* ne
       return fail(PGSR_ERANGE, "crop of sequence %d to %d tokens; it holds %d", seqs[i], L, len);
   }
   rc = do_crop(p, n, seqs, new_lens, flags, (hipStream_t)stream);
+  if (!rc) rc = device_check(p, (hipStream_t)stream);
   return rc ? rc : ok();
 }
 
@@ -893,7 +939,9 @@ int pgsr_kv_fork(pgsr_pool* p, int32_t n, const int32_t* srcs, const int32_t* ds
     a.tables = p->tables;
     a.lens = p->lens;
     a.refs = p->refs;
+    a.chk = p->chk;
     a.max_bps = p->max_bps;
+    a.n_blocks = p->n_blocks;
     a.n = cnt;
     for (int32_t i = 0; i < cnt; ++i) {
       const int32_t s = srcs[base + i], d = dsts[base + i];
@@ -909,7 +957,8 @@ int pgsr_kv_fork(pgsr_pool* p, int32_t n, const int32_t* srcs, const int32_t* ds
     hipError_t err = launch_fork(a, st);
     if (err != hipSuccess) return hip_fail(err, "fork launch");
   }
-  return ok();
+  rc = device_check(p, st);
+  return rc ? rc : ok();
 }
 
 int pgsr_replay_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seqs,
@@ -945,6 +994,7 @@ int replay_prefill_ws(pgsr_pool* p, int32_t layer, int32_t n, const int32_t* seq
   if (rc) return rc;
   rc = do_replay(p, layer, n, seqs, q_lens, q, k, v, o, softmax_scale, flags, recomputed_tokens, ws,
                  ws_bytes, (hipStream_t)stream);
+  if (!rc) rc = device_check(p, (hipStream_t)stream);
   return rc ? rc : ok();
 }
 
@@ -964,8 +1014,9 @@ int pgsr_full_reset_prefill(pgsr_pool* p, int32_t layer, int32_t n, const int32_
   if (n > 0 && (!seqs || !lens)) return fail(PGSR_EINVAL, "null seqs / lens");
   // layer 0: restore every sequence to 0 tokens, then replay the whole trajectory
   std::vector<int32_t> zeros(n, 0);
-  const int rc = restore_replay(p, layer, n, seqs, layer == 0 ? zeros.data() : nullptr, lens, q, k, v, o,
-                                softmax_scale, flags, recomputed_tokens, (hipStream_t)stream);
+  int rc = restore_replay(p, layer, n, seqs, layer == 0 ? zeros.data() : nullptr, lens, q, k, v, o,
+                          softmax_scale, flags, recomputed_tokens, (hipStream_t)stream);
+  if (!rc) rc = device_check(p, (hipStream_t)stream);
   return rc ? rc : ok();
 }
 
@@ -977,8 +1028,9 @@ int pgsr_restore_replay_prefill(pgsr_pool* p, int32_t layer, int32_t n, const in
   if (n < 0) return fail(PGSR_EINVAL, "n = %d", n);
   if (flags & ~(unsigned)PGSR_COMMIT) return fail(PGSR_EINVAL, "unknown replay flags 0x%x", flags);
   if (n > 0 && (!seqs || !restore_lens || !q_lens)) return fail(PGSR_EINVAL, "null seqs / lens");
-  const int rc = restore_replay(p, layer, n, seqs, restore_lens, q_lens, q, k, v, o, softmax_scale,
-                                flags, recomputed_tokens, (hipStream_t)stream);
+  int rc = restore_replay(p, layer, n, seqs, restore_lens, q_lens, q, k, v, o, softmax_scale, flags,
+                          recomputed_tokens, (hipStream_t)stream);
+  if (!rc) rc = device_check(p, (hipStream_t)stream);
   return rc ? rc : ok();
 }
 

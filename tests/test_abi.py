@@ -36,6 +36,18 @@ def test_every_declared_symbol_is_exported(native):
     assert set(names) == set(native.EXPORTS)
 
 
+def test_checked_build_exports_the_same_symbols(native):
+    """The checked build (block ids validated on the device) has the same C ABI."""
+    path = os.path.join(os.path.dirname(native.LIB_PATH), "libpgsr_checked.so")
+    if not os.path.exists(path):
+        pytest.skip("checked build not built")
+    raw = ctypes.CDLL(path)
+    missing = [n for n in declared_functions() if not hasattr(raw, n)]
+    assert not missing, missing
+    raw.pgsr_abi_version.restype = ctypes.c_int
+    assert raw.pgsr_abi_version() == native.lib.pgsr_abi_version()
+
+
 def test_abi_version_and_workspace_size(native):
     assert native.lib.pgsr_abi_version() == 2
     assert native.lib.pgsr_workspace_bytes(32, 128, 2048, 4) == 2048 * 32 * 4 * 130 * 4
