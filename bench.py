@@ -160,6 +160,18 @@ class Setup:
         return sum(attention_bytes(p, s, g.n_q_heads, g.n_kv_heads, g.head_dim, eb)
                    for p, s in zip(self.P, self.S))
 
+    def prefix_bytes(self) -> float:
+        """K/V bytes of the keys before each replay call's first query (the
+        cropped prefix; for a chunked replay, the prefix grown so far, read
+        once per chunk)."""
+        g = self.w.geometry
+        eb = 4 if self.w.dtype == "f32" else 2
+        per_key = 2.0 * g.n_kv_heads * g.head_dim * eb
+        if self.chunk:
+            P, S, C = self.P[0], self.S[0], self.chunk
+            return per_key * sum(P + c0 for c0 in range(0, S, C))
+        return per_key * sum(self.P)
+
 
 def host_cpu() -> dict:
     """The host the CPU baseline ran on: model name, sockets, physical cores
@@ -731,6 +743,7 @@ def main() -> int:
     # mean shader clock of the timed attention dispatches of this run (cycle and
     # reference counters read by every workgroup at its start and end)
     sclk = clk_cycles / clk_ticks * clk_rate if clk_ticks else None
+    traffic = measured_traffic(kfile, w.name)
     # crop: released table entries (each read, cleared, its count read and
     # written, then pushed) plus lengths and the stack top
     released = sum(-(-e.t_contaminated // w.block_size) - -(-e.prefix // w.block_size) for e in st.eps)
@@ -756,7 +769,7 @@ def main() -> int:
                    "recomputed_tokens": sum(st.S)},
         "roofline": {"bound": "mfma" if w.dtype == "bf16" else "alu", "achieved": achieved,
                      "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": measured_traffic(kfile, w.name),
+                     "traffic": traffic,
                      # the clock the kernel ran at in this run's instrumented pass and
                      # the fraction of the peak at that clock (peak scales with sclk / 2.4);
                      # a diagnostic: frac is taken at the nominal 2.4 GHz
@@ -768,13 +781,18 @@ def main() -> int:
                                 else f"attn_f32_kernel<{g.head_dim}>"),
                      "flops_per_step": flops, "algorithmic_bytes_per_step": nbytes,
                      "kernel_ms": attn_mean, "kernel_launches_per_step": st.calls_per_step,
-                     "algorithmic_GBps": nbytes / (attn_mean * 1e-3) / 1e9},
+                     "algorithmic_GBps": nbytes / (attn_mean * 1e-3) / 1e9,
+                     # HBM rates over the kernel time: the cropped prefix's K/V
+                     # (algorithmic) and the counted traffic (committed counters)
+                     "prefix_GBps": st.prefix_bytes() / (attn_mean * 1e-3) / 1e9,
+                     "traffic_GBps": (None if traffic is None else traffic / (attn_mean * 1e-3) / 1e9)},
         "crop": {"us": float(np.mean(crop_ms)) * 1e3, "algorithmic_bytes": crop_bytes,
                  "released_blocks": released},
         "breakdown_ms": {"crop_call": float(np.mean(crop_ms)),
                          "restore_append": float(np.mean(append_ms)),
                          "attention": attn_mean, "step": total_s * 1e3 / args.steps,
                          "step_min": float(np.min(step_ms)),
+                         "step_median": float(np.median(step_ms)),
                          "step_instrumented": float(np.mean(inst_ms)) if inst_ms else None},
     }
     if not args.no_cpu_baseline:
