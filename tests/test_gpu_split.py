@@ -93,9 +93,14 @@ def test_long_horizon_split_full_size_sampled():
     pool = make_pool(w.geometry, "bf16", _blocks(36864) + 8, 1, 2400, split_q=w.chunk)
     contaminated_then_crop(pool, ep, 0, w.scale)
     o = _chunked(pool, ep, w.chunk, w.scale)
+    # every chunk's first two and last two tokens and 96 random ones, all 32
+    # query heads of each (4096 of the 131,072 output rows)
     rng = np.random.default_rng(7)
-    toks = np.unique(np.concatenate([[0, 1, 511, 512, 4095], rng.integers(0, 4096, 40)]))
-    rows = np.unique(np.concatenate([toks * 32 + rng.integers(0, 32, toks.shape[0]), toks * 32 + 31]))
+    edges = [c + x for c in range(0, 4096, w.chunk) for x in (0, 1, w.chunk - 2, w.chunk - 1)]
+    rest = np.setdiff1d(np.arange(4096), edges)
+    toks = np.sort(np.concatenate([edges, rng.choice(rest, 96, replace=False)]))
+    rows = (toks[:, None] * 32 + np.arange(32)[None, :]).reshape(-1)
+    log(f"oracle on {rows.size} rows ({toks.size} tokens x 32 heads)")
     ref = oracle_suffix(ep, w.scale, rows=rows)
     assert_close(o.float().cpu().numpy().reshape(-1, 128)[rows], ref, "bf16", w.name)
 
