@@ -513,6 +513,8 @@ def bench_decode(args):
     import torch
     from paper_2609_04875_amd import BF16, FP8_E4M3, KVPool, sample_tokens, sample_workspace_bytes, workspace_bytes
     fp8 = args.workload.endswith("_fp8")
+    # "decode" names the bf16 workload in full (its profiles carry the full name)
+    name = "decode_llama8b_b32_ctx8192" + ("_fp8" if fp8 else "")
     n, ctx, hq, hkv, d, B, vocab, T = 32, 8192, 32, 8, 128, 16, 128256, 0.7
     kv_elem = 1 if fp8 else 2
     # warm-up, the timed steps, then as many instrumented steps for the kernel time
@@ -566,12 +568,12 @@ def bench_decode(args):
         "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": total_s * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": args.workload, "sequences": n, "context": ctx,
+        "config": {"workload": name, "sequences": n, "context": ctx,
                    "n_q_heads": hq, "n_kv_heads": hkv, "head_dim": d, "block_size": B, "vocab": vocab,
                    "temperature": T, "kv_cache": "e4m3" if fp8 else "bf16"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": 8000.0, "unit": "GB/s",
                      "frac": achieved / 8000.0,
-                     "traffic": measured_traffic("attn_decode", args.workload),
+                     "traffic": measured_traffic("attn_decode", name),
                      "kernel": f"attn_decode_kernel<128,16,{'fp8' if fp8 else 'bf16'}> + split_combine_kernel<128>",
                      "kernel_ms": a_ms, "kernel_launches_per_step": 1,
                      "algorithmic_bytes_per_step": float(np.mean(kv_bytes))},
