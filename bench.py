@@ -8,7 +8,8 @@ contaminated cache of 10240 tokens cropped to 8189 (not a multiple of the
 16-token block) and a 2048-token suffix replayed against it.  ``--workload``
 selects the other workloads (tiny fp32 episode, 16 ragged episodes in one
 varlen launch, 32k-prefix chunked replay, the 8-layer stacked workload, 4 full
-decoder layers at the 8B geometry (``llama8b_4layer_decoder_t8192_bf16``),
+decoder layers at the 8B geometry (``llama8b_4layer_decoder_t8192_bf16``; the
+paper's episode scale on all 32 layers, ``paper_t1330_llama8b_32layer_bf16``),
 ``decode``: one-token steps over 32 cached sequences with seeded sampling,
 and ``frontend``: the host-side forget queries that produce the crop length).  Inputs are seeded synthetic
 tensors resident in HBM before timing starts.
@@ -404,14 +405,27 @@ def copy_calibration(mib: int) -> None:
 def bench_decoder(args):
     """Full decoder layers at the Llama-3.1-8B geometry (d_model 4096, 32/8
     heads, d 128, d_ff 14336; RMSNorm, rotary embedding at absolute positions,
-    SwiGLU MLP), 4 layers, T = 8192 random-init tokens: crop + replay of the
-    suffix from tau - 1 = 50 % and 75 % of T through every layer, against the
-    full reset of all T tokens.  The roofline is the dominant kernel, the fused
-    gate/up projection (S x 28672 x 4096)."""
+    SwiGLU MLP), random-init weights, crop + replay of the suffix from each
+    restore point through every layer, against the full reset of all T
+    tokens.  ``llama8b_4layer_decoder_t8192_bf16``: 4 layers, T = 8192, restore
+    points at 50 % and 75 % of T.  ``paper_t1330_llama8b_32layer_bf16``: the
+    paper's episode scale (full resets of about 1.2k-1.3k tokens in its
+    Table 1 and its sweep of the injection turn) on all 32 layers, T = 1330,
+    restore points
+    at 13 equally spaced turn boundaries (round(k T / 13), k = 0 .. 12; k = 0
+    is the full reset itself).  The roofline is the dominant kernel, the fused
+    gate/up projection (S x 28672 x 4096, S the longest replayed suffix)."""
     import torch
     from paper_2609_04875_amd import DecoderReplay, gemm_bf16
-    L, dm, hq, hkv, d, dff, T, eps, theta = 4, 4096, 32, 8, 128, 14336, 8192, 1e-5, 5e5
-    g = torch.Generator(device="cuda").manual_seed(11)
+    dm, hq, hkv, d, dff, eps, theta = 4096, 32, 8, 128, 14336, 1e-5, 5e5
+    paper = args.workload.startswith("paper_t1330")
+    if paper:
+        L, T, seed = 32, 1330, 12
+        prefixes = [round(k * T / 13) for k in range(13)]
+    else:
+        L, T, seed = 4, 8192, 11
+        prefixes = [int(0.5 * T), int(0.75 * T)]
+    g = torch.Generator(device="cuda").manual_seed(seed)
     rnd = lambda *shape, s=1.0: (torch.randn(*shape, device="cuda", generator=g) * s).to(torch.bfloat16)
     ws = [{"wq": rnd(hq * d, dm, s=dm ** -0.5), "wk": rnd(hkv * d, dm, s=dm ** -0.5),
            "wv": rnd(hkv * d, dm, s=dm ** -0.5), "wo": rnd(dm, hq * d, s=(hq * d) ** -0.5),
@@ -437,11 +451,26 @@ def bench_decoder(args):
         return ms
 
     reps = max(1, args.steps // 4)
+    empty = pool.save_meta()
     full_ms = timed(lambda: dec.full_reset(1, x0), reps)
+    # the full reset recorded as a HIP graph too (restore to an empty sequence
+    # + replay of all T tokens), checked bit for bit against the eager call
+    full_eager = dec.full_reset(1, x0).clone()
+    pool.load_meta(empty)
+    capf = dec.capture_restore_replay(1, 0, x0)
+    full_gms = []
+    for i in range(args.warmup + reps):
+        pool.load_meta(empty)
+        m = timed(capf.replay, 1)[0]
+        if not torch.equal(capf.output, full_eager):
+            raise RuntimeError("graph full reset differs from the eager one")
+        if i >= args.warmup:
+            full_gms.append(m)
+    pool.load_meta(empty)
+    del capf
     flops_tok = 2.0 * dm * (hq + 2 * hkv) * d + 2.0 * hq * d * dm + 2.0 * dm * 3 * dff
     points = []
-    for frac in (0.5, 0.75):
-        P = int(frac * T)
+    for P in prefixes:
         S = T - P
         pool.crop([0], [0])
         dec.replay(0, torch.cat([x0[:P], xc[P:]]))        # contaminated run into the cache
@@ -458,11 +487,32 @@ def bench_decoder(args):
             m = timed(step, 1)[0]
             if i >= args.warmup:
                 ms.append(m)
+        # the same restore + replay recorded once as a HIP graph (the host's
+        # per-call work leaves the timed region), replayed from the restored
+        # state; every replay must give the eager replay's bits
+        pool.load_meta(saved)
+        dec.crop([0], [P])
+        eager = dec.replay(0, xs).clone()
+        pool.load_meta(saved)
+        cap = dec.capture_restore_replay(0, P, xs)
+        gms = []
+        for i in range(args.warmup + reps):
+            pool.load_meta(saved)
+            m = timed(cap.replay, 1)[0]
+            if not torch.equal(cap.output, eager):
+                raise RuntimeError("graph replay differs from the eager replay")
+            if i >= args.warmup:
+                gms.append(m)
+        pool.load_meta(saved)
+        del cap
         fl = (flops_tok * S + attention_flops(P, S, hq, d)) * L
         points.append({"prefix": P, "recomputed_tokens": S, "token_ratio": T / S,
                        "replay_ms": float(np.mean(ms)), "full_reset_ms": float(np.mean(full_ms)),
                        "wall_time_ratio": float(np.mean(full_ms) / np.mean(ms)),
-                       "replay_TFLOPs": fl / (np.mean(ms) * 1e-3) / 1e12})
+                       "replay_TFLOPs": fl / (np.mean(ms) * 1e-3) / 1e12,
+                       "replay_graph_ms": float(np.mean(gms)),
+                       "full_reset_graph_ms": float(np.mean(full_gms)),
+                       "wall_time_ratio_graph": float(np.mean(full_gms) / np.mean(gms))})
     S = T - points[0]["prefix"]
     h = rnd(S, dm)
     gu = torch.empty((S, 2 * dff), dtype=torch.bfloat16, device="cuda")
@@ -475,9 +525,9 @@ def bench_decoder(args):
         "n_gpus": 1, "steps": reps, "warmup": args.warmup, "ms_per_step": total_ms / len(points),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "llama8b_4layer_decoder_t8192_bf16", "t_total": T, "layers": L,
+        "config": {"workload": args.workload, "t_total": T, "layers": L,
                    "d_model": dm, "d_ff": dff, "n_q_heads": hq, "n_kv_heads": hkv, "head_dim": d,
-                   "prefix_fracs": [0.5, 0.75], "block_size": 16, "rope_theta": theta, "rms_eps": eps},
+                   "prefixes": prefixes, "block_size": 16, "rope_theta": theta, "rms_eps": eps},
         "roofline": {"bound": "mfma", "achieved": gflops / (gemm_ms * 1e-3) / 1e12,
                      "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
                      "frac": gflops / (gemm_ms * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"], "traffic": None,
@@ -490,13 +540,13 @@ def bench_decoder(args):
         layers = [{"wq": f64(w["wq"]).T, "wk": f64(w["wk"]).T, "wv": f64(w["wv"]).T, "wo": f64(w["wo"]).T,
                    "wg": f64(w["w_gate_up"][:dff]).T, "wu": f64(w["w_gate_up"][dff:]).T,
                    "wd": f64(w["w_down"]).T, "g_attn": f64(w["g_attn"]), "g_mlp": f64(w["g_mlp"])} for w in ws]
-        n = 32
+        n = 4 if paper else 32
         t0 = time.perf_counter()
         DEC.decoder_layers(f64(x0[:n]), layers, hq, hkv, d, eps, theta)
         dt = time.perf_counter() - t0
         import oracle
         result["cpu_baseline"] = {"value": n / dt, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
-                                  "sample": f"{n} tokens from position 0 through the 4 layers"}
+                                  "sample": f"{n} tokens from position 0 through the {L} layers"}
     print(json.dumps(result), flush=True)
     return 0
 
@@ -684,7 +734,7 @@ def main() -> int:
         return bench_stack(args)
     if args.workload.startswith("decode"):
         return bench_decode(args)
-    if args.workload.startswith("llama8b_4layer_decoder"):
+    if args.workload.startswith("llama8b_4layer_decoder") or args.workload.startswith("paper_t1330"):
         return bench_decoder(args)
     st = Setup(args.workload)
     w, g, pool = st.w, st.w.geometry, st.pool

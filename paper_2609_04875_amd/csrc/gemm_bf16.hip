@@ -7,7 +7,9 @@
 //
 // A workgroup computes a BM x BN output tile with WGM x WGN waves, each wave a
 // (TM * 32) x (TN * 32) block as (2 TM) x (2 TN) 16 x 16 MFMA tiles: 128 x 128
-// with 4 waves of 64 x 64, two workgroups per CU.  K advances 64 at a time
+// with 4 waves of 64 x 64, two workgroups per CU; products with fewer than
+// 128 such tiles take 128 x 32 (two waves) or, up to 64 rows, 64 x 32 (one
+// wave) tiles, so that more workgroups stream W at once.  K advances 64 at a time
 // through padded, double-buffered LDS tiles of X rows and W rows (both
 // k-contiguous, so both MFMA operands are 16-byte reads); the next K steps
 // are loaded into registers while the current one is multiplied.  The
@@ -187,8 +189,17 @@ void launch_tiles(int m, int n, int k, const void* x, const void* w, const void*
 hipError_t launch_gemm_bf16(int m, int n, int k, const void* x, const void* w, const void* r,
                             void* y, hipStream_t s) {
   if (gemm_bf16_wide_eligible(m, n, k)) return launch_gemm_bf16_wide(m, n, k, x, w, r, y, s);
-  // every other product: 128 x 128 tiles, two workgroups per CU
-  launch_tiles<2, 2, 2, 2, 2>(m, n, k, x, w, r, y, s);
+  const int64_t tiles128 = (int64_t)((m + 127) / 128) * ((n + 127) / 128);
+  if (tiles128 < 128) {
+    // 128 x 128 tiles would leave most CUs idle (few rows: a short replayed
+    // suffix against a model's weights): 32-column tiles, four times as many
+    // workgroups streaming W at once; 64 x 32 for at most 64 rows
+    if (m <= 64) launch_tiles<1, 1, 2, 1, 4>(m, n, k, x, w, r, y, s);
+    else launch_tiles<2, 1, 2, 1, 3>(m, n, k, x, w, r, y, s);
+  } else {
+    // every other product: 128 x 128 tiles, two workgroups per CU
+    launch_tiles<2, 2, 2, 2, 2>(m, n, k, x, w, r, y, s);
+  }
   return hipGetLastError();
 }
 

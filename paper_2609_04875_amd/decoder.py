@@ -109,3 +109,45 @@ class DecoderReplay:
 
     def crop(self, seqs: List[int], new_lens: List[int]) -> int:
         return self.pool.crop(seqs, new_lens)
+
+    def capture_restore_replay(self, seq: int, crop_len: int, x: torch.Tensor) -> "CapturedReplay":
+        """Record the restore (crop of ``seq`` to ``crop_len``) and the replay
+        of ``x`` through every layer as one HIP graph, from the pool state at
+        this call.  Every library call of the two steps only enqueues kernels
+        (no allocation, copy or memset on the stream), so the graph holds the
+        launches the calls made, with the block ids the host mirror chose for
+        that state.  Nothing runs during the capture: afterwards the host
+        mirror reflects the recorded calls while the device is unchanged.
+        Replaying is valid only from the captured state: restore it (device
+        tables and host mirror, e.g. ``pool.load_meta``) before each replay."""
+        n = x.shape[0]
+        # scratch and positions allocated outside the capture
+        for name, shape in (("h", (n, self.d_model)), ("q", (n, self.hq, self.d)), ("k", (n, self.hkv, self.d)),
+                            ("v", (n, self.hkv, self.d)), ("o", (n, self.hq * self.d)),
+                            ("gu", (n, 2 * self.d_ff)), ("a", (n, self.d_ff))):
+            self._scratch(name, *shape)
+        xin = x.clone()
+        stream = torch.cuda.Stream()
+        stream.wait_stream(torch.cuda.current_stream())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            with torch.cuda.graph(graph, stream=stream):
+                rc = self.crop([seq], [crop_len])
+                if rc:
+                    raise N.PgsrError(rc, N.lib.pgsr_last_error().decode())
+                out = self._run(self.pool.replay, seq, xin, crop_len)
+        torch.cuda.current_stream().wait_stream(stream)
+        return CapturedReplay(graph, xin, out)
+
+
+class CapturedReplay:
+    """A restore + replay recorded by DecoderReplay.capture_restore_replay:
+    ``input`` holds the replayed token states (overwrite it in place to replay
+    others), ``output`` receives the result of each ``replay()``."""
+
+    def __init__(self, graph: "torch.cuda.CUDAGraph", inp: torch.Tensor, out: torch.Tensor):
+        self.graph, self.input, self.output = graph, inp, out
+
+    def replay(self) -> torch.Tensor:
+        self.graph.replay()
+        return self.output

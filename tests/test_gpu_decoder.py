@@ -100,3 +100,42 @@ def test_decoder_replay_matches_oracle_and_full_reset(hq, hkv, d):
     # magnitude, L1-relative 1e-2 (as for the stacked layers)
     assert diff.max() <= 2.0 ** -6 * np.abs(want).max(), (diff.max(), np.abs(want).max())
     assert diff.sum() / np.abs(want).sum() <= 1e-2
+
+
+def test_captured_restore_replay_matches_eager():
+    """Restore + replay through two layers recorded as one HIP graph: three
+    replays, each from the restored contaminated state with eager library work
+    in between, give the eager replay's bits every time."""
+    log("decoder restore + replay as a HIP graph")
+    hq, hkv, d = 4, 2, 64
+    rng = np.random.default_rng(99)
+    dm, dff, T, P, Tc = hq * d, 384, 300, 203, 330
+    eps, theta = 1e-5, 5e5
+    ws = _weights(rng, 2, dm, hq, hkv, d, dff)
+    x = bf16_round(rng.standard_normal((T, dm)))
+    xc = np.concatenate([x[:P], bf16_round(rng.standard_normal((Tc - P, dm)))])
+    dec = DecoderReplay(_dev_weights(ws), hq, hkv, d, eps, theta, n_blocks=3 * (-(-Tc // 16)) + 8,
+                        max_seqs=2, max_blocks_per_seq=32)
+    dec.replay(0, _dev(xc))
+    torch.cuda.synchronize()
+    saved = dec.pool.save_meta()
+    assert dec.crop([0], [P]) == 0
+    want = dec.replay(0, _dev(x[P:])).clone()
+    torch.cuda.synchronize()
+    after = dec.pool.save_meta()
+
+    dec.pool.load_meta(saved)
+    cap = dec.capture_restore_replay(0, P, _dev(x[P:]))
+    for i in range(3):
+        dec.pool.load_meta(saved)
+        got = cap.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(got, want), f"graph replay {i} differs from the eager replay"
+        assert all(torch.equal(a, b) for a, b in zip(dec.pool.save_meta(), after)), f"replay {i} tables"
+        # eager work between replays: a full reset of another sequence
+        dec.pool.refresh()
+        full = dec.full_reset(1, _dev(x))
+        torch.cuda.synchronize()
+        assert torch.equal(full[P:], want)
+        assert dec.crop([1], [0]) == 0
+        torch.cuda.synchronize()

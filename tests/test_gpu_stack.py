@@ -77,6 +77,21 @@ def test_gemm_tile_shapes_agree_bitwise():
     assert torch.equal(part, full[1000:1300])
 
 
+@pytest.mark.parametrize("rows", [(101, 201), (7, 70), (0, 1), (40, 168)])
+def test_gemm_narrow_tiles_agree_bitwise(rows):
+    """Few rows (64 x 32 or 128 x 32 tiles) against the same rows inside a
+    larger product (128 x 128 tiles): same bits; K not a multiple of 64."""
+    from paper_2609_04875_amd import gemm_bf16
+    rng = np.random.default_rng(6)
+    x = _bf16_dev(rng.standard_normal((4096, 1000)))       # 32 x 9 tiles of 128 x 128
+    w = _bf16_dev(rng.standard_normal((1048, 1000)) / 32)
+    r = _bf16_dev(rng.standard_normal((4096, 1048)))
+    full = gemm_bf16(x, w, r=r)
+    a, b = rows
+    part = gemm_bf16(x[a:b].contiguous(), w, r=r[a:b].contiguous())
+    assert torch.equal(part, full[a:b])
+
+
 @pytest.mark.parametrize("m,n,k", [(64, 128, 256), (4096, 4096, 128)])   # both kernels
 def test_gemm_residual_may_alias_output(m, n, k):
     from paper_2609_04875_amd import gemm_bf16
