@@ -121,23 +121,30 @@ class DecoderReplay:
         Replaying is valid only from the captured state: restore it (device
         tables and host mirror, e.g. ``pool.load_meta``) before each replay."""
         n = x.shape[0]
-        # scratch and positions allocated outside the capture
-        for name, shape in (("h", (n, self.d_model)), ("q", (n, self.hq, self.d)), ("k", (n, self.hkv, self.d)),
-                            ("v", (n, self.hkv, self.d)), ("o", (n, self.hq * self.d)),
-                            ("gu", (n, 2 * self.d_ff)), ("a", (n, self.d_ff))):
-            self._scratch(name, *shape)
-        xin = x.clone()
-        stream = torch.cuda.Stream()
-        stream.wait_stream(torch.cuda.current_stream())
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.stream(stream):
-            with torch.cuda.graph(graph, stream=stream):
-                rc = self.crop([seq], [crop_len])
-                if rc:
-                    raise N.PgsrError(rc, N.lib.pgsr_last_error().decode())
-                out = self._run(self.pool.replay, seq, xin, crop_len)
-        torch.cuda.current_stream().wait_stream(stream)
-        return CapturedReplay(graph, xin, out)
+        # scratch of its own, allocated before the capture and owned by the
+        # result: the graph keeps these addresses, so eager calls that later
+        # grow the shared scratch must not free them
+        shared, self._buf = self._buf, {}
+        try:
+            for name, shape in (("h", (n, self.d_model)), ("q", (n, self.hq, self.d)),
+                                ("k", (n, self.hkv, self.d)), ("v", (n, self.hkv, self.d)),
+                                ("o", (n, self.hq * self.d)), ("gu", (n, 2 * self.d_ff)), ("a", (n, self.d_ff))):
+                self._scratch(name, *shape)
+            xin = x.clone()
+            stream = torch.cuda.Stream()
+            stream.wait_stream(torch.cuda.current_stream())
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(stream):
+                with torch.cuda.graph(graph, stream=stream):
+                    rc = self.crop([seq], [crop_len])
+                    if rc:
+                        raise N.PgsrError(rc, N.lib.pgsr_last_error().decode())
+                    out = self._run(self.pool.replay, seq, xin, crop_len)
+            torch.cuda.current_stream().wait_stream(stream)
+            own = self._buf
+        finally:
+            self._buf = shared
+        return CapturedReplay(graph, xin, out, own)
 
 
 class CapturedReplay:
@@ -145,8 +152,9 @@ class CapturedReplay:
     ``input`` holds the replayed token states (overwrite it in place to replay
     others), ``output`` receives the result of each ``replay()``."""
 
-    def __init__(self, graph: "torch.cuda.CUDAGraph", inp: torch.Tensor, out: torch.Tensor):
-        self.graph, self.input, self.output = graph, inp, out
+    def __init__(self, graph: "torch.cuda.CUDAGraph", inp: torch.Tensor, out: torch.Tensor,
+                 scratch: Dict[str, torch.Tensor]):
+        self.graph, self.input, self.output, self._scratch = graph, inp, out, scratch
 
     def replay(self) -> torch.Tensor:
         self.graph.replay()
