@@ -45,16 +45,17 @@ __device__ inline u32x4 zero_tail(u32x4 v, int pos0, int limit) {
   return v;
 }
 
-// Eight E4M3 codes (byte e = element e) as eight bf16 values, exactly: the
-// hardware conversion gives fp32 pairs, whose upper halves are the bf16 bits.
+// Eight E4M3 codes (byte e = element e) as eight bf16 values, exactly (a
+// code has at most 4 significant bits and an exponent inside bf16's range):
+// the scaled pair conversion with scale 1 widens two codes per instruction
+// (bytes 0-1 or 2-3 of a word).  On all 65536 pairs of codes it gives the
+// bits of the fp32 pair conversion's upper halves, NaNs included.
 __device__ inline u32x4 widen_fp8(u32x2 w) {
   u32x4 r;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[h], false);   // bytes 0, 1
-    const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[h], true);    // bytes 2, 3
-    r[2 * h] = __builtin_amdgcn_perm(__float_as_uint(lo[1]), __float_as_uint(lo[0]), 0x07060302u);
-    r[2 * h + 1] = __builtin_amdgcn_perm(__float_as_uint(hi[1]), __float_as_uint(hi[0]), 0x07060302u);
+    r[2 * h] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[h], 1.0f, false));
+    r[2 * h + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[h], 1.0f, true));
   }
   return r;
 }
