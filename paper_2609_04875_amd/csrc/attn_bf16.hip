@@ -386,7 +386,7 @@ constexpr int kGroup = 8;
 template <int D, typename TO>
 __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, TO* __restrict__ og) {
   constexpr int TPR = D / 8;                       // threads per row
-  const int64_t row = a.row_begin + (int64_t)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+  const int64_t row = a.row_begin + (int64_t)blockIdx.x * (blockDim.x / TPR) + threadIdx.x / TPR;
   const int c0 = (threadIdx.x % TPR) * 8;
   if (row >= a.row_end) return;
   const int tok = (int)(row / a.n_q_heads);        // packed query token
@@ -402,7 +402,32 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, TO* __re
   // Indices past the last split are clamped to it (always a valid address)
   // and weighted 0, so each group's loads are unconditional and issue together.
   float M = -INFINITY;
-  for (int s0 = 0; s0 < ns; s0 += kGroup) {
+  float L = 0.f;
+  f32x4 o0 = {0, 0, 0, 0}, o1 = {0, 0, 0, 0};
+  if (ns <= kGroup) {
+    // one group (every decode call): all loads in one round trip, then the
+    // same max, weights and sums in the same order as the general loop below
+    float mg[kGroup], lg[kGroup];
+    f32x4 a0[kGroup], a1[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+      const int64_t prow = (int64_t)min(j, ns - 1) * a.n_rows + row;
+      mg[j] = ml[2 * prow];
+      lg[j] = ml[2 * prow + 1];
+      a0[j] = *(const f32x4*)(acc + prow * D + c0);
+      a1[j] = *(const f32x4*)(acc + prow * D + c0 + 4);
+    }
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) M = fmaxf(M, mg[j]);
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+      const float wgt = j < ns ? __builtin_amdgcn_exp2f(mg[j] - M) : 0.f;
+      L = fmaf(wgt, lg[j], L);
+      o0 += wgt * a0[j];
+      o1 += wgt * a1[j];
+    }
+  }
+  for (int s0 = 0; s0 < ns && ns > kGroup; s0 += kGroup) {
     float mg[kGroup];
 #pragma unroll
     for (int j = 0; j < kGroup; ++j)
@@ -410,9 +435,7 @@ __global__ void __launch_bounds__(256) split_combine_kernel(AttnArgs a, TO* __re
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) M = fmaxf(M, mg[j]);
   }
-  float L = 0.f;
-  f32x4 o0 = {0, 0, 0, 0}, o1 = {0, 0, 0, 0};
-  for (int s0 = 0; s0 < ns; s0 += kGroup) {
+  for (int s0 = 0; s0 < ns && ns > kGroup; s0 += kGroup) {
     float mg[kGroup], lg[kGroup];
     f32x4 a0[kGroup], a1[kGroup];
 #pragma unroll
@@ -473,16 +496,21 @@ static hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
 hipError_t launch_split_combine(const AttnArgs& a, bool f32_out, hipStream_t s) {
   if (a.row_begin < 0 || a.row_end > a.n_rows) return hipErrorInvalidValue;
   if (a.row_end <= a.row_begin) return hipSuccess;
-  const int rows_per_block = 256 / (a.head_dim / 8);
-  dim3 grid((a.row_end - a.row_begin + rows_per_block - 1) / rows_per_block);
+  // 256 threads per block, or 64 when that would leave CUs idle (decode
+  // calls have a few thousand rows)
+  const int64_t rows = a.row_end - a.row_begin;
+  const int tpr = a.head_dim / 8;
+  const int threads = (rows + 256 / tpr - 1) / (256 / tpr) >= 1024 ? 256 : 64;
+  const int rows_per_block = threads / tpr;
+  dim3 grid((rows + rows_per_block - 1) / rows_per_block);
   if (a.head_dim == 128 && f32_out)
-    hipLaunchKernelGGL((split_combine_kernel<128, float>), grid, dim3(256), 0, s, a, (float*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<128, float>), grid, dim3(threads), 0, s, a, (float*)a.o);
   else if (a.head_dim == 64 && f32_out)
-    hipLaunchKernelGGL((split_combine_kernel<64, float>), grid, dim3(256), 0, s, a, (float*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<64, float>), grid, dim3(threads), 0, s, a, (float*)a.o);
   else if (a.head_dim == 128)
-    hipLaunchKernelGGL((split_combine_kernel<128, uint16_t>), grid, dim3(256), 0, s, a, (uint16_t*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<128, uint16_t>), grid, dim3(threads), 0, s, a, (uint16_t*)a.o);
   else if (a.head_dim == 64)
-    hipLaunchKernelGGL((split_combine_kernel<64, uint16_t>), grid, dim3(256), 0, s, a, (uint16_t*)a.o);
+    hipLaunchKernelGGL((split_combine_kernel<64, uint16_t>), grid, dim3(threads), 0, s, a, (uint16_t*)a.o);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
